@@ -1,0 +1,196 @@
+// Token GEMMs C[M,N] = A[M,K] . W[N,K]^T with fused epilogues (bias, GELU,
+// residual add into the fp32 stream, patch-embedding scatter, fp32 logits).
+//
+// bf16 path: MFMA v_mfma_f32_32x32x16_bf16 on 128x128 tiles staged through
+// LDS, fp32 accumulation.  fp32 path: LDS-tiled VALU FMA (no rounding).
+// Rows are the packed live tokens of all samples, so ragged lengths are
+// invisible here: M is read from the device counters and the grid is sized
+// for an upper bound (tiles past M return at once).
+#include "kernels.h"
+
+namespace fusion {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+template <typename T>
+__device__ __forceinline__ void epilogue(const Epi& e, int r, int n, float acc) {
+  switch (e.mode) {
+    case EPI_STORE:
+      ((T*)e.out)[(size_t)r * e.ldo + n] = St<T>::put(acc + e.bias[n]);
+      break;
+    case EPI_GELU:
+      ((T*)e.out)[(size_t)r * e.ldo + n] = St<T>::put(gelu_erf(acc + e.bias[n]));
+      break;
+    case EPI_RESID: {
+      float* p = (float*)e.out + (size_t)r * e.ldo + n;
+      *p = *p + (acc + e.bias[n]);
+      break;
+    }
+    case EPI_F32: {
+      const int orow = e.rows ? e.rows[r] : r;
+      ((float*)e.out)[(size_t)orow * e.ldo + n] = acc + e.bias[n];
+      break;
+    }
+    case EPI_PATCH: {
+      const int s = r / e.n0, j = r - s * e.n0;
+      const size_t xr = (size_t)s * (e.n0 + 1) + 1 + j;
+      ((float*)e.out)[xr * e.ldo + n] =
+          (acc + e.bias[n]) + e.pos[(size_t)(1 + j) * e.ldo + n];
+      break;
+    }
+  }
+}
+
+// ------------------------------------------------------------ fp32 VALU --
+template <typename T>
+__global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
+                                                 int lda,
+                                                 const T* __restrict__ W,
+                                                 int N, int K,
+                                                 const int* M_dev, int M_host,
+                                                 Epi e) {
+  const int M = M_dev ? *M_dev : M_host;
+  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64;
+  if (m0 >= M) return;
+  __shared__ float As[16][68];
+  __shared__ float Ws[16][68];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; i++)
+#pragma unroll
+    for (int j = 0; j < 4; j++) acc[i][j] = 0.f;
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    for (int idx = threadIdx.x; idx < 64 * 16; idx += 256) {
+      const int r = idx >> 4, kk = idx & 15;
+      const int gk = k0 + kk;
+      const int gr = m0 + r, gn = n0 + r;
+      As[kk][r] = (gr < M && gk < K) ? St<T>::get(A[(size_t)gr * lda + gk]) : 0.f;
+      Ws[kk][r] = (gn < N && gk < K) ? St<T>::get(W[(size_t)gn * K + gk]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; kk++) {
+      float a[4], w[4];
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        a[i] = As[kk][ty * 4 + i];
+        w[i] = Ws[kk][tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) acc[i][j] = fmaf(a[i], w[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const int r = m0 + ty * 4 + i;
+    if (r >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int n = n0 + tx * 4 + j;
+      if (n < N) epilogue<T>(e, r, n, acc[i][j]);
+    }
+  }
+}
+
+// ------------------------------------------------------------ bf16 MFMA --
+// 256 threads = 4 waves in a 2x2 grid; each wave owns a 64x64 sub-tile made
+// of 2x2 MFMA 32x32 blocks.  A and W tiles are [128][BK] bf16 in LDS with a
+// padded row stride (BK + 8) so that the 16-byte per-lane operand reads of
+// consecutive rows fall in different banks.
+//
+// Operand layout of v_mfma_f32_32x32x16_bf16 (64 lanes): lane l supplies
+// A[row l%32][k 8*(l/32) .. +7] and B[k 8*(l/32) .. +7][col l%32]; result
+// element q of lane l is C[8*(q/4) + 4*(l/32) + q%4][l%32].
+constexpr int MB = 128, NB = 128, KB = 64, KP = KB + 8;
+
+__global__ __launch_bounds__(256) void gemm_mfma_bf16(
+    const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
+    int N, int K, const int* M_dev, int M_host, Epi e) {
+  const int M = M_dev ? *M_dev : M_host;
+  const int m0 = blockIdx.x * MB, n0 = blockIdx.y * NB;
+  if (m0 >= M) return;
+  __shared__ __attribute__((aligned(16))) bf16_t As[MB * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[NB * KP];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; i++)
+#pragma unroll
+    for (int j = 0; j < 2; j++)
+#pragma unroll
+      for (int q = 0; q < 16; q++) acc[i][j][q] = 0.f;
+
+  for (int k0 = 0; k0 < K; k0 += KB) {
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+      const int chunk = tid + c * 256;
+      const int r = chunk >> 3, kc = (chunk & 7) * 8;
+      uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
+      if (m0 + r < M) va = *(const uint4*)(A + (size_t)(m0 + r) * lda + k0 + kc);
+      if (n0 + r < N) vb = *(const uint4*)(W + (size_t)(n0 + r) * K + k0 + kc);
+      *(uint4*)(As + r * KP + kc) = va;
+      *(uint4*)(Bs + r * KP + kc) = vb;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < KB; ks += 16) {
+      bf16x8_t a[2], b[2];
+      const int ko = ks + (lane >> 5) * 8;
+#pragma unroll
+      for (int i = 0; i < 2; i++)
+        a[i] = *(const bf16x8_t*)(As + (wm * 64 + i * 32 + (lane & 31)) * KP + ko);
+#pragma unroll
+      for (int j = 0; j < 2; j++)
+        b[j] = *(const bf16x8_t*)(Bs + (wn * 64 + j * 32 + (lane & 31)) * KP + ko);
+#pragma unroll
+      for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 2; i++)
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+      if (n >= N) continue;
+#pragma unroll
+      for (int q = 0; q < 16; q++) {
+        const int r = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+        if (r < M) epilogue<bf16_t>(e, r, n, acc[i][j][q]);
+      }
+    }
+}
+
+template <>
+hipError_t launch_gemm<float>(const float* A, int lda, const float* W, int N,
+                              int K, const int* M_dev, int M_host, int M_ub,
+                              const Epi& e, hipStream_t s) {
+  if (M_ub <= 0) return hipSuccess;
+  dim3 grid((M_ub + 63) / 64, (N + 63) / 64);
+  gemm_valu<float><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, e);
+  return hipGetLastError();
+}
+
+template <>
+hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
+                               int N, int K, const int* M_dev, int M_host,
+                               int M_ub, const Epi& e, hipStream_t s) {
+  if (M_ub <= 0) return hipSuccess;
+  // The MFMA tiles need K % 64 == 0 and 16-byte aligned rows; the model
+  // creation rejects bf16 shapes that do not satisfy this.
+  if (K % KB != 0 || lda % 8 != 0) return hipErrorInvalidValue;
+  dim3 grid((M_ub + MB - 1) / MB, (N + NB - 1) / NB);
+  gemm_mfma_bf16<<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, e);
+  return hipGetLastError();
+}
+
+}  // namespace fusion

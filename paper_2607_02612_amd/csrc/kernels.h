@@ -1,0 +1,133 @@
+// Host-side launchers of the gfx950 kernels (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace fusion {
+
+// Epilogue of the token GEMMs  C[M,N] = A[M,K] . W[N,K]^T.
+enum EpiMode {
+  EPI_STORE = 0,  // out(T)[r, n]  = acc + bias[n]
+  EPI_GELU = 1,   // out(T)[r, n]  = GELU(acc + bias[n])
+  EPI_RESID = 2,  // x(f32)[r, n]  = x[r, n] + (acc + bias[n])
+  EPI_F32 = 3,    // out(f32)[rows ? rows[r] : r, n] = acc + bias[n]
+  EPI_PATCH = 4   // x(f32)[s (n0+1) + 1 + j, n] = (acc + bias[n]) + pos[1 + j, n],
+                  //   r = s n0 + j
+};
+
+struct Epi {
+  int mode;
+  void* out;
+  int ldo;
+  const float* bias;
+  const int* rows;  // EPI_F32 scatter map (optional)
+  const float* pos; // EPI_PATCH
+  int n0;           // EPI_PATCH
+};
+
+// Row count: *M_dev when non-null, else M_host.  M_ub bounds the grid.
+template <typename T>
+hipError_t launch_gemm(const T* A, int lda, const T* W, int N, int K,
+                       const int* M_dev, int M_host, int M_ub, const Epi& e,
+                       hipStream_t s);
+
+template <typename T>
+hipError_t launch_patchify(const float* img, T* out, int B, int C, int S,
+                           int p, hipStream_t s);
+
+// State at the start of a run: unit sizes, origin ids, cu/live maps, CLS
+// rows of x, zeroed token counts.
+hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
+                       LiveCounts* cnt, int* token_counts, const float* cls,
+                       const float* pos, int B, int n0, int d, int L,
+                       hipStream_t s);
+
+// LayerNorm of packed rows (cls_only = 0: rows 0..M-1 -> out rows 0..M-1;
+// cls_only = 1: row cu[i] of live sample i -> out row i).  When exit_block is
+// non-null (final head), also writes exit_block[live[i]] = L.
+template <typename T>
+hipError_t launch_layernorm(const float* x, const float* g, const float* b,
+                            T* out, int d, const LiveCounts* cnt,
+                            const int* cu, const int* live, int cls_only,
+                            int rows_ub, int* exit_block, int L, hipStream_t s);
+
+struct AttnArgs {
+  const void* qkv;  // T [M, 3d]
+  const float* size;
+  const int* cu;
+  const int* live;
+  const LiveCounts* cnt;
+  int H, dh, d;
+  float scale;
+  int prop_attn;
+  void* out;           // T [M, d]
+  float* cls_scores;   // [nlive, H, tmax] or null
+  int tmax;
+  int* token_counts;   // [B, L]: written for head 0
+  int L, b0;           // layers, 0-based block
+  int nlive_ub, T_ub;
+};
+template <typename T>
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+struct AdaptArgs {
+  float* x;
+  float* size;
+  const int* origin;
+  const int* cu;
+  const int* live;
+  const LiveCounts* cnt;
+  int d, H, n0, C, L, B;
+  int b;  // 1-based block
+  int isM, isE, isP;
+  const float* router_w;
+  const float* router_b;
+  int r_b;
+  double rho;
+  const float* head_buf;  // [nlive, C] exit-head logits
+  float delta;
+  float* logits;
+  int* exit_block;
+  const float* cls_scores;
+  int tmax;
+  double tau_eff;
+  int* keep;    // [M] row flags
+  int* newlen;  // [nlive]
+  int* tr_r;
+  float* tr_m;
+  float* tr_c;
+  int* tr_merge;
+  int nlive_ub;
+};
+hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s);
+
+struct CompactArgs {
+  const float* x;
+  const float* size;
+  const int* origin;
+  const int* cu;
+  const int* live;
+  const LiveCounts* cnt;
+  const int* keep;
+  const int* newlen;
+  float* x2;
+  float* size2;
+  int* origin2;
+  int* cu2;
+  int* live2;
+  LiveCounts* cnt2;
+  int d, n0, B, b;
+  int* tr_ids;
+  int nlive_ub;
+};
+hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
+
+// Copy of the packed state for diagnostics.
+hipError_t launch_copy_state(const float* x, const int* cu, const int* live,
+                             const LiveCounts* cnt, float* x_out, int* cu_out,
+                             int* live_out, int d, int rows_ub, int nlive_ub,
+                             hipStream_t s);
+
+}  // namespace fusion

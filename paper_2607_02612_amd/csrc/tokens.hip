@@ -1,0 +1,175 @@
+// Token-level kernels: run initialisation, patch extraction (Eq. 1),
+// LayerNorm of packed rows (pre-norm blocks, exit and final heads), and a
+// diagnostic state copy.
+#include "kernels.h"
+
+namespace fusion {
+
+__global__ void init_kernel(float* __restrict__ x, float* __restrict__ size,
+                            int* __restrict__ origin, int* __restrict__ cu,
+                            int* __restrict__ live, LiveCounts* cnt,
+                            int* __restrict__ token_counts,
+                            const float* __restrict__ cls,
+                            const float* __restrict__ pos, int B, int n0,
+                            int d, int L) {
+  const int T0 = n0 + 1;
+  const long rows = (long)B * T0;
+  const long total = rows > (long)B * L ? rows : (long)B * L;
+  const long cls_elems = (long)B * d;
+  const long stride = (long)gridDim.x * blockDim.x;
+  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+       t < (total > cls_elems ? total : cls_elems); t += stride) {
+    if (t < rows) {
+      size[t] = 1.0f;
+      origin[t] = (int)(t % T0);
+    }
+    if (t < (long)B * L) token_counts[t] = 0;
+    if (t < cls_elems) {
+      const int s = (int)(t / d), n = (int)(t - (long)s * d);
+      x[(size_t)s * T0 * d + n] = cls[n] + pos[n];
+    }
+    if (t <= B) cu[t] = (int)(t * T0);
+    if (t < B) live[t] = (int)t;
+    if (t == 0) {
+      cnt->nlive = B;
+      cnt->M = (int)rows;
+    }
+  }
+}
+
+hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
+                       LiveCounts* cnt, int* token_counts, const float* cls,
+                       const float* pos, int B, int n0, int d, int L,
+                       hipStream_t s) {
+  long work = (long)B * (n0 + 1);
+  if ((long)B * d > work) work = (long)B * d;
+  if ((long)B * L > work) work = (long)B * L;
+  int blocks = (int)((work + 255) / 256);
+  if (blocks > 4096) blocks = 4096;
+  init_kernel<<<blocks, 256, 0, s>>>(x, size, origin, cu, live, cnt,
+                                     token_counts, cls, pos, B, n0, d, L);
+  return hipGetLastError();
+}
+
+// images [B, C, S, S] -> patches [B*n0, C*p*p]; patch (gy, gx) in raster
+// order, vector element (c, ky, kx).
+template <typename T>
+__global__ void patchify_kernel(const float* __restrict__ img, T* __restrict__ out,
+                                int B, int C, int S, int p) {
+  const int g = S / p, n0 = g * g, pd = C * p * p;
+  const long total = (long)B * n0 * pd;
+  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < total;
+       t += (long)gridDim.x * blockDim.x) {
+    const long row = t / pd;
+    const int e = (int)(t - row * pd);
+    const int s = (int)(row / n0), j = (int)(row - (long)s * n0);
+    const int gy = j / g, gx = j - gy * g;
+    const int c = e / (p * p), rem = e - c * p * p;
+    const int ky = rem / p, kx = rem - ky * p;
+    const float v = img[(((size_t)s * C + c) * S + gy * p + ky) * S + gx * p + kx];
+    out[t] = St<T>::put(v);
+  }
+}
+
+template <typename T>
+hipError_t launch_patchify(const float* img, T* out, int B, int C, int S,
+                           int p, hipStream_t s) {
+  const long total = (long)B * (S / p) * (S / p) * C * p * p;
+  int blocks = (int)((total + 255) / 256);
+  if (blocks > 16384) blocks = 16384;
+  patchify_kernel<T><<<blocks, 256, 0, s>>>(img, out, B, C, S, p);
+  return hipGetLastError();
+}
+template hipError_t launch_patchify<float>(const float*, float*, int, int, int, int, hipStream_t);
+template hipError_t launch_patchify<bf16_t>(const float*, bf16_t*, int, int, int, int, hipStream_t);
+
+// One wave per row: mean and biased variance in fp32 (two passes over the
+// row held in registers), y = (x - mean) / sqrt(var + 1e-6) * g + b.
+template <typename T>
+__global__ __launch_bounds__(256) void layernorm_kernel(
+    const float* __restrict__ x, const float* __restrict__ g,
+    const float* __restrict__ bb, T* __restrict__ out, int d,
+    const LiveCounts* cnt, const int* __restrict__ cu,
+    const int* __restrict__ live, int cls_only, int* exit_block, int L) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + wave;
+  const int nrows = cls_only ? cnt->nlive : cnt->M;
+  if (row >= nrows) return;
+  const size_t src = cls_only ? (size_t)cu[row] : (size_t)row;
+  const float* xr = x + src * d;
+  constexpr int MAXV = 12;  // d <= 768
+  float v[MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; i++) {
+    const int n = lane + i * 64;
+    v[i] = n < d ? xr[n] : 0.f;
+    s += v[i];
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; i++) {
+    const int n = lane + i * 64;
+    const float c = n < d ? v[i] - mean : 0.f;
+    q += c * c;
+  }
+  const float var = wave_sum(q) / (float)d;
+  const float rstd = 1.0f / sqrtf(var + 1e-6f);
+  T* o = out + (size_t)row * d;
+#pragma unroll
+  for (int i = 0; i < MAXV; i++) {
+    const int n = lane + i * 64;
+    if (n < d) o[n] = St<T>::put(((v[i] - mean) * rstd) * g[n] + bb[n]);
+  }
+  if (exit_block && lane == 0) exit_block[live[row]] = L;
+}
+
+template <typename T>
+hipError_t launch_layernorm(const float* x, const float* g, const float* b,
+                            T* out, int d, const LiveCounts* cnt,
+                            const int* cu, const int* live, int cls_only,
+                            int rows_ub, int* exit_block, int L,
+                            hipStream_t s) {
+  if (rows_ub <= 0) return hipSuccess;
+  if (d > 768) return hipErrorInvalidValue;
+  layernorm_kernel<T><<<(rows_ub + 3) / 4, 256, 0, s>>>(
+      x, g, b, out, d, cnt, cu, live, cls_only, exit_block, L);
+  return hipGetLastError();
+}
+template hipError_t launch_layernorm<float>(const float*, const float*, const float*, float*, int,
+                                            const LiveCounts*, const int*, const int*, int, int,
+                                            int*, int, hipStream_t);
+template hipError_t launch_layernorm<bf16_t>(const float*, const float*, const float*, bf16_t*,
+                                             int, const LiveCounts*, const int*, const int*, int,
+                                             int, int*, int, hipStream_t);
+
+__global__ void copy_state_kernel(const float* __restrict__ x, const int* cu,
+                                  const int* live, const LiveCounts* cnt,
+                                  float* __restrict__ x_out, int* cu_out,
+                                  int* live_out, int d) {
+  const int nl = cnt->nlive;
+  const long n = (long)cnt->M * d;
+  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < n;
+       t += (long)gridDim.x * blockDim.x)
+    x_out[t] = x[t];
+  const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t <= nl) cu_out[t] = cu[t];
+  if (t < nl) live_out[t] = live[t];
+}
+
+hipError_t launch_copy_state(const float* x, const int* cu, const int* live,
+                             const LiveCounts* cnt, float* x_out, int* cu_out,
+                             int* live_out, int d, int rows_ub, int nlive_ub,
+                             hipStream_t s) {
+  long work = (long)rows_ub * d;
+  int blocks = (int)((work + 255) / 256);
+  const int need = (nlive_ub + 1 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < need) blocks = need;
+  copy_state_kernel<<<blocks, 256, 0, s>>>(x, cu, live, cnt, x_out, cu_out,
+                                           live_out, d);
+  return hipGetLastError();
+}
+
+}  // namespace fusion

@@ -1,0 +1,105 @@
+"""Helpers shared by the GPU parity tests: run the HIP path through the C ABI
+and check every sample against the CPU oracle, letting the oracle follow the
+GPU only at decisions whose oracle margin is below 1e-3 (near ties)."""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+from oracle import fusion_oracle as fo
+from synth import blob, configs, images, weights
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def mode_of(cfg):
+    return "fp32" if cfg["precision"] == "fp32" else "bf16emu"
+
+
+def logit_tol(cfg):
+    return 1e-4 if cfg["precision"] == "fp32" else 2e-2
+
+
+def exit_thresholds(name, rho):
+    with open(os.path.join(GOLDEN, "exit_thresholds.json")) as f:
+        data = json.load(f)
+    for w in data["workloads"]:
+        if w["workload"] == name and w["rho"] == rho:
+            return {float(k): v for k, v in w["thresholds"].items()}
+    raise KeyError((name, rho))
+
+
+def make(name, batch=None, affine="plain", router_std=0.02, **over):
+    cfg = configs.get(name, **over)
+    W = weights.make_weights(cfg, affine=affine, router_std=router_std)
+    imgs = images.make_images(cfg, batch=batch or cfg["batch"])
+    return cfg, W, imgs
+
+
+def gpu_model(cfg, W, max_batch):
+    from paper_2607_02612_amd import FusionModel
+    return FusionModel(blob.pack(cfg, W), max_batch)
+
+
+def gpu_run(model, imgs_dev, delta=None, rho=1.0, traced=True):
+    import torch
+    if delta is not None:
+        model.set_exit_thresholds(delta)
+    model.set_router_strength(rho)
+    B = imgs_dev.shape[0]
+    tr = model.alloc_trace(B) if traced else None
+    lg, eb, cnt = model.run(imgs_dev, trace=tr)
+    torch.cuda.synchronize()
+    out = dict(logits=lg.cpu().numpy(), exit_block=eb.cpu().numpy(),
+               counts=cnt.cpu().numpy())
+    if traced:
+        out["trace"] = {k: v.cpu().numpy() for k, v in tr.items()}
+    return out
+
+
+def follow_of(cfg, res, i):
+    """The GPU's decisions for sample i in the oracle's follow format."""
+    tr = res["trace"]
+    f = {}
+    for b in range(1, cfg["L"] + 1):
+        if res["counts"][i][b - 1] == 0:
+            break
+        if not (b in cfg["merges"] or b in cfg["exits"] or b in cfg["prunes"]):
+            continue
+        md = tr["merge_dst"][b - 1, i]
+        merge = {int(s): int(t) for s, t in enumerate(md) if t >= 0}
+        row = tr["ids"][b - 1, i]
+        n = int((row >= 0).sum())
+        f[b] = dict(r=int(tr["r"][b - 1, i]) if b in cfg["merges"] else 0,
+                    merge=merge,
+                    exit=bool(b in cfg["exits"] and res["exit_block"][i] == b),
+                    ids=row[:n].tolist())
+    return f
+
+
+def check_samples(cfg, W, imgs, res, idx, delta=None, rho=1.0):
+    """Oracle (follow mode) on samples idx; asserts decisions, counts and
+    logits; returns (max |dlogit|, adopted near-tie decisions, details)."""
+    mode = mode_of(cfg)
+    Wp = fo.prepare_weights(W, mode)
+    tol = logit_tol(cfg)
+    worst, adopted = 0.0, []
+    for i in idx:
+        out = fo.run_sample(imgs[i], Wp, cfg, mode, delta=delta, rho=rho,
+                            follow=follow_of(cfg, res, i))
+        assert out["exit_block"] == res["exit_block"][i], i
+        assert np.array_equal(out["token_counts"], res["counts"][i]), (
+            i, out["token_counts"], res["counts"][i])
+        err = float(np.abs(out["logits"] - res["logits"][i]).max())
+        assert err <= tol, (i, err)
+        worst = max(worst, err)
+        adopted += [(int(i),) + a for a in out["adopted"]]
+        tr = res["trace"]
+        for b, tb in out["trace"].items():
+            if "m" in tb:
+                assert abs(tb["m"] - tr["m"][b - 1, i]) < 1e-4, (i, b)
+            if "c" in tb:
+                assert abs(tb["c"] - tr["c"][b - 1, i]) < 2e-3, (i, b, tb["c"], tr["c"][b - 1, i])
+    return worst, adopted

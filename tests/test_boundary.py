@@ -1,0 +1,115 @@
+"""C-ABI boundary checks that need no GPU: the library loads, exports every
+declared entry point, and rejects malformed blobs and arguments on the host
+with the documented status codes."""
+import ctypes
+import os
+import re
+import struct
+
+import numpy as np
+import pytest
+
+from paper_2607_02612_amd import _native
+from paper_2607_02612_amd.model import blob_inspect
+from synth import blob, configs, weights
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "fusion.h")) as f:
+        txt = f.read()
+    return re.findall(r"FUSION_API\s+[\w\s\*]+?\b(fusion_\w+)\s*\(", txt)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _native.lib()
+    names = _declared()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    assert {n for n, _, _ in _native.SIGNATURES} == set(names)
+
+
+@pytest.fixture(scope="module")
+def tiny_blob():
+    cfg = configs.get("tiny")
+    return cfg, blob.pack(cfg, weights.make_weights(cfg))
+
+
+def test_blob_inspect_reads_header(tiny_blob):
+    cfg, b = tiny_blob
+    info = blob_inspect(b)
+    assert info["d"] == cfg["d"] and info["layers"] == cfg["L"]
+    assert info["n0"] == cfg["N0"] and info["classes"] == cfg["C"]
+    assert info["exit_blocks"] == list(cfg["exits"])
+    assert info["precision"] == 0
+    assert info["r_b"] == list(cfg["r_b"])
+    assert info["delta"] == pytest.approx(list(cfg["delta"]))
+    cfg3 = configs.get("deit_s")
+    info3 = blob_inspect(blob.pack(cfg3, weights.make_weights(cfg3)))
+    assert info3["precision"] == 1 and info3["exit_blocks"] == [4, 8]
+    assert info3["tau_b"][3] == 0.7 and info3["tau_b"][0] == 1.0
+
+
+def _expect(code, b):
+    lib = _native.lib()
+    info = _native.FusionInfo()
+    rc = lib.fusion_blob_inspect(b, len(b), ctypes.byref(info))
+    assert rc == code, (rc, lib.fusion_last_error())
+    assert lib.fusion_last_error().decode() != ""
+    return lib.fusion_last_error().decode()
+
+
+def test_corrupt_blobs_are_rejected(tiny_blob):
+    cfg, b = tiny_blob
+    E = -2
+    _expect(E, b"\0" * 10)
+    _expect(E, b"XXXXXXXX" + b[8:])                       # magic
+    _expect(E, b[:8] + struct.pack("<I", 7) + b[12:])     # version
+    _expect(E, b[:1000])                                   # truncated data
+    # a tensor shape that disagrees with the header
+    d_off = 16 + 4 * 3
+    bad = bytearray(b)
+    bad[d_off:d_off + 4] = struct.pack("<I", cfg["d"] * 2)
+    assert "shape" in _expect(E, bytes(bad))
+    # exit mask naming a block beyond L
+    bad = bytearray(b)
+    bad[60:64] = struct.pack("<I", 1 << 20)
+    _expect(E, bytes(bad))
+    # keep ratio outside [0, 1]
+    bad = bytearray(b)
+    bad[196:204] = struct.pack("<d", 1.5)
+    _expect(E, bytes(bad))
+    # tensor name out of order
+    bad = bytearray(b)
+    nm = 584
+    bad[nm:nm + 3] = b"xyz"
+    assert "expected tensor" in _expect(E, bytes(bad))
+
+
+def test_create_rejects_bad_arguments_before_touching_device(tiny_blob):
+    cfg, b = tiny_blob
+    lib = _native.lib()
+    h = ctypes.c_void_p()
+    assert lib.fusion_model_create(b, len(b), 0, ctypes.byref(h)) == -1
+    assert lib.fusion_model_create(b, len(b), 1 << 20, ctypes.byref(h)) == -1
+    assert lib.fusion_model_create(b"junk" * 200, 800, 4, ctypes.byref(h)) == -2
+    assert lib.fusion_model_create(None, 0, 4, ctypes.byref(h)) == -1
+    assert lib.fusion_model_create(b, len(b), 4, None) == -1
+    assert lib.fusion_model_destroy(None) == -1
+    assert lib.fusion_set_router_strength(None, 1.0) == -1
+    assert lib.fusion_run(None, None, 1, None, None, None, None) == -1
+
+
+def test_bf16_shape_limits_are_checked():
+    cfg = configs.get("deit_ti", mlp=700)   # not a multiple of 64
+    b = blob.pack(cfg, weights.make_weights(cfg))
+    assert "multiples of 64" in _expect(-2, b)
+
+
+def test_profile_kind_names():
+    lib = _native.lib()
+    n = lib.fusion_profile_kinds()
+    names = [lib.fusion_profile_kind_name(k).decode() for k in range(n)]
+    assert "attention" in names and "adapt" in names and len(set(names)) == n

@@ -1,0 +1,153 @@
+"""End-to-end GPU parity of the staged pipeline (merge -> exit -> prune) with
+the CPU oracle, through the C ABI (fusion_run_traced).
+
+Every compared sample must take the oracle's decisions (merge pairs, r,
+exit block, kept token ids, token counts) except at decisions whose oracle
+margin is below 1e-3, where the oracle adopts the GPU's choice after
+checking it is one of the near-tied options; logits must agree within 1e-4
+(fp32 workload) or 2e-2 (bf16 workloads).  Full-size workloads are run at
+their whole batch on the GPU and sampled for the oracle (each sample is
+independent of the rest of the batch).
+"""
+import numpy as np
+import pytest
+
+import parity_utils as pu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _report(tag, worst, adopted, n):
+    print(f"[{tag}] samples={n} max|dlogit|={worst:.3e} near-tie adoptions={len(adopted)}",
+          flush=True)
+
+
+@pytest.mark.parametrize("affine,router_std", [("plain", 0.02), ("random", 0.2)])
+def test_tiny_fp32_all_samples(torch_cuda, affine, router_std):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("tiny", affine=affine, router_std=router_std)
+    print(f"[tiny fp32] affine={affine}", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda())
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]))
+    _report("tiny", worst, adopted, cfg["batch"])
+
+
+@pytest.mark.parametrize("affine,router_std,rho", [("plain", 0.02, 1.0),
+                                                   ("random", 0.2, 1.0),
+                                                   ("plain", 0.02, 1.5)])
+def test_deit_ti_bf16_all_samples(torch_cuda, affine, router_std, rho):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_ti", affine=affine, router_std=router_std)
+    print(f"[deit_ti] affine={affine} router_std={router_std} rho={rho}", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), rho=rho)
+    n_exit = int((res["exit_block"] < cfg["L"]).sum())
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]), rho=rho)
+    _report("deit_ti", worst, adopted, cfg["batch"])
+    print(f"  early exits {n_exit}/{cfg['batch']}")
+
+
+@pytest.mark.parametrize("e", [0.0, 0.5, 0.9])
+def test_deit_s_full_batch_sampled(torch_cuda, e):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_s")
+    delta = pu.exit_thresholds("deit_s", 1.0)[e]
+    print(f"[deit_s b256] e={e} delta={delta}", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[delta, delta])
+    n_early = int((res["exit_block"] < cfg["L"]).sum())
+    # the oracle's calibration makes round(e B) samples exit early; a
+    # near-tie at the threshold may move one sample
+    assert abs(n_early - round(e * cfg["batch"])) <= 1
+    idx = [0, 1, 77, 128, 200, 255]
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, idx, delta=[delta, delta])
+    _report("deit_s", worst, adopted, len(idx))
+
+
+def test_deit_b_full_batch_sampled(torch_cuda):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_b")
+    print("[deit_b b256]", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda())
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, [0, 131, 255])
+    _report("deit_b", worst, adopted, 3)
+
+
+@pytest.mark.parametrize("rho", [0.5, 1.0, 1.5])
+def test_deit_s_384_sampled(torch_cuda, rho):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_s_384")
+    delta = pu.exit_thresholds("deit_s_384", rho)[0.5]
+    print(f"[deit_s_384 b64] rho={rho} delta={delta}", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[delta, delta], rho=rho)
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, [0, 33, 63],
+                                      delta=[delta, delta], rho=rho)
+    _report("deit_s_384", worst, adopted, 3)
+
+
+def test_plain_vit_special_case(torch_cuda):
+    """delta = 1, rho = 0: no merge, exit or prune; equals the plain ViT."""
+    torch = torch_cuda
+    from oracle import fusion_oracle as fo
+    cfg, W, imgs = pu.make("deit_ti", batch=8, affine="random")
+    m = pu.gpu_model(cfg, W, 8)
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[1.0, 1.0], rho=0.0)
+    assert np.all(res["counts"] == cfg["N0"] + 1)
+    assert np.all(res["exit_block"] == cfg["L"])
+    Wp = fo.prepare_weights(W, "bf16emu")
+    for i in range(8):
+        ref = fo.plain_forward(imgs[i], Wp, cfg, "bf16emu")
+        assert np.abs(ref - res["logits"][i]).max() <= 2e-2
+
+
+def test_threshold_zero_exits_at_first_head(torch_cuda):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("tiny")
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[0.0])
+    assert np.all(res["exit_block"] == cfg["exits"][0])
+    assert np.all(res["counts"][:, cfg["exits"][0]:] == 0)
+
+
+def test_determinism_permutation_and_isolation(torch_cuda):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_ti", batch=16)
+    m = pu.gpu_model(cfg, W, 16)
+    x = torch.from_numpy(imgs).cuda()
+    a = pu.gpu_run(m, x)
+    b = pu.gpu_run(m, x)
+    for k in ("logits", "exit_block", "counts"):
+        assert np.array_equal(a[k], b[k]), k
+    perm = np.random.default_rng(0).permutation(16)
+    c = pu.gpu_run(m, torch.from_numpy(np.ascontiguousarray(imgs[perm])).cuda())
+    for k in ("logits", "exit_block", "counts"):
+        assert np.array_equal(c[k], a[k][perm]), k
+    one = pu.gpu_run(m, torch.from_numpy(imgs[5:6].copy()).cuda())
+    assert np.array_equal(one["logits"][0], a["logits"][5])
+    assert np.array_equal(one["counts"][0], a["counts"][5])
+
+
+def test_capacity_and_argument_errors(torch_cuda):
+    torch = torch_cuda
+    from paper_2607_02612_amd import FusionError
+    cfg, W, imgs = pu.make("tiny")
+    m = pu.gpu_model(cfg, W, 4)
+    with pytest.raises(FusionError) as ei:
+        m.run(torch.from_numpy(imgs).cuda())
+    assert ei.value.code == -3
+    with pytest.raises(FusionError) as ei:
+        m.set_exit_thresholds([0.5, 0.5])
+    assert ei.value.code == -1
+    with pytest.raises(FusionError):
+        m.set_router_strength(-1.0)
