@@ -45,9 +45,9 @@ Readings of the paper where it is silent (each also listed in the design doc):
       order kept; only samples that did not exit (Eq. 8, Sec. III-B).
 
 Decision margins (in O(1) units) are logged for every discrete decision:
-argmax best - second similarity, top-r gap s_(r) - s_(r+1), router distance
-of 2 rho m r_b + 1/2 to the nearest integer (unclamped only), exit |c - delta|,
-prune N (s_(k) - s_(k+1)).
+argmax best - second similarity, top-r gap s_(r) - s_(r+1), router: the
+change of m that moves 2 rho m r_b + 1/2 across an integer (unclamped
+only), exit |c - delta|, prune N (s_(k) - s_(k+1)).
 
 Follow mode: given another implementation's decisions (``follow``), the
 oracle checks each against its own and adopts it only when the disagreement
@@ -70,6 +70,34 @@ from scipy.special import erf as _erf
 
 F32 = np.float32
 TOL = 1e-3
+
+# Accumulation of the matrix products: "fp32" (BLAS sgemm, the default) or
+# "fp64" (accumulate in double, round once to float32).  Only the summation
+# order differs; the second setting measures how far the bf16 rounding points
+# amplify summation-order noise (a property of the arithmetic, not of any
+# implementation).
+ACCUM = "fp32"
+
+
+def _mm(a, b):
+    if ACCUM == "fp64":
+        return (np.asarray(a, np.float64) @ np.asarray(b, np.float64)).astype(F32)
+    return a @ b
+
+
+class accumulate:
+    """Context manager selecting ACCUM for the oracle's matrix products."""
+
+    def __init__(self, mode):
+        self.mode = mode
+
+    def __enter__(self):
+        global ACCUM
+        self.prev, ACCUM = ACCUM, self.mode
+
+    def __exit__(self, *exc):
+        global ACCUM
+        ACCUM = self.prev
 
 
 class DecisionMismatch(AssertionError):
@@ -129,7 +157,7 @@ def patchify(img, p):
 def patch_embed(img, W, cfg, mode):
     """z_0 = [cls; patches W_pe^T + b_pe] + pos (Eq. 1)."""
     P = _rnd(patchify(img, cfg["patch"]), mode)
-    tok = P @ W["pe_w"].T + W["pe_b"]
+    tok = _mm(P, W["pe_w"].T) + W["pe_b"]
     z = np.concatenate([W["cls"][None, :], tok], axis=0)
     return (z + W["pos"]).astype(F32)
 
@@ -145,7 +173,7 @@ def attention(x, s, Wb, cfg, mode, want_cls):
     d, H = cfg["d"], cfg["H"]
     dh = d // H
     h = _rnd(layer_norm(x, Wb["ln1_g"], Wb["ln1_b"]), mode)
-    qkv = _rnd(h @ Wb["qkv_w"].T + Wb["qkv_b"], mode)
+    qkv = _rnd(_mm(h, Wb["qkv_w"].T) + Wb["qkv_b"], mode)
     scale = F32(1.0 / math.sqrt(dh))
     bias = np.log(s).astype(F32) if cfg["prop_attn"] else None
     T = x.shape[0]
@@ -155,12 +183,12 @@ def attention(x, s, Wb, cfg, mode, want_cls):
         q = qkv[:, hh * dh:(hh + 1) * dh]
         k = qkv[:, d + hh * dh:d + (hh + 1) * dh]
         v = qkv[:, 2 * d + hh * dh:2 * d + (hh + 1) * dh]
-        S = (q @ k.T) * scale
+        S = _mm(q, k.T) * scale
         if bias is not None:
             S = S + bias[None, :]
         E = np.exp(S - S.max(axis=1, keepdims=True))
         l = E.sum(axis=1, keepdims=True, dtype=F32)
-        O[:, hh * dh:(hh + 1) * dh] = (_rnd(E, mode) @ v) / l
+        O[:, hh * dh:(hh + 1) * dh] = _mm(_rnd(E, mode), v) / l
         if want_cls:
             cls_rows.append(E[0] / l[0])
     cls_attn = None
@@ -175,17 +203,17 @@ def attention(x, s, Wb, cfg, mode, want_cls):
 def block(x, s, Wb, cfg, mode, want_cls=False):
     """Block_b: x += proj(MHSA(LN1 x)); x += fc2(GELU(fc1(LN2 x))) (Eq. 2)."""
     O, cls_attn = attention(x, s, Wb, cfg, mode, want_cls)
-    x = x + (O @ Wb["proj_w"].T + Wb["proj_b"])
+    x = x + (_mm(O, Wb["proj_w"].T) + Wb["proj_b"])
     h = _rnd(layer_norm(x, Wb["ln2_g"], Wb["ln2_b"]), mode)
-    f = _rnd(gelu(h @ Wb["fc1_w"].T + Wb["fc1_b"]), mode)
-    x = x + (f @ Wb["fc2_w"].T + Wb["fc2_b"])
+    f = _rnd(gelu(_mm(h, Wb["fc1_w"].T) + Wb["fc1_b"]), mode)
+    x = x + (_mm(f, Wb["fc2_w"].T) + Wb["fc2_b"])
     return x.astype(F32), cls_attn
 
 
 def head_logits(x_cls, g, b, Wh, bh, mode):
     """Linear classifier on LN(CLS) (Eq. 3 and the exit heads of Eq. 6)."""
     y = _rnd(layer_norm(x_cls[None, :], g, b), mode)
-    return (y @ Wh.T + bh)[0].astype(F32)
+    return (_mm(y, Wh.T) + bh)[0].astype(F32)
 
 
 def max_softmax(l):
@@ -198,15 +226,18 @@ def max_softmax(l):
 def router(x_cls, w, beta, rho, r_b, N):
     """m = sigmoid(w . z_cls + beta) (Eq. 4); r from the rho-scaled budget.
 
-    Returns (m, r, margin); margin is the distance of 2 rho m r_b + 1/2 to
-    the nearest integer, +inf when the count is clamped.
+    Returns (m, r, margin).  The margin is in units of m, like every other
+    decision margin in O(1) units: the distance of 2 rho m r_b + 1/2 to the
+    nearest integer divided by 2 rho r_b, i.e. how far m must move to change
+    r; +inf when the count is clamped or does not depend on m.
     """
     z = F32(np.dot(w, x_cls)) + F32(beta)
     m = F32(1.0) / (F32(1.0) + np.exp(-z, dtype=F32))
     t = ((2.0 * float(rho)) * float(m)) * float(r_b) + 0.5
     r_raw = math.floor(t)
     r = min(max(r_raw, 0), N // 2)
-    margin = abs(t - round(t)) if r == r_raw else math.inf
+    slope = 2.0 * float(rho) * float(r_b)
+    margin = abs(t - round(t)) / slope if (r == r_raw and slope > 0) else math.inf
     return m, int(r), margin
 
 
@@ -319,9 +350,16 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
     follow: optional per-block dict {b: {"r": int, "merge": {src_origin:
             dst_origin}, "exit": bool, "ids": [origin ids after the block's
             adaptation]}} from another implementation (see module doc).
+    tol:    decision margin under which a followed choice may differ; a
+            float, or {"exit": t_exit, "other": t} to give the exit rule its
+            own margin (in units of c).
     Returns dict(logits, exit_block, token_counts[L], trace, adopted).
     """
     L = cfg["L"]
+    if isinstance(tol, dict):
+        tol_exit, tol = tol["exit"], tol["other"]
+    else:
+        tol_exit = tol
     if delta is None:
         delta = cfg["delta"]
     delta_of = {b: F32(dl) for b, dl in zip(cfg["exits"], delta)}
@@ -376,7 +414,7 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
             tb.update(c=float(c), exit_margin=abs(float(c) - float(dl)),
                       exit_logits=lg)
             if fb is not None and fb["exit"] != fire:
-                if not abs(float(c) - float(dl)) < tol:
+                if not abs(float(c) - float(dl)) < tol_exit:
                     raise DecisionMismatch(f"block {b}: exit {fb['exit']} vs oracle {fire} (c={c}, delta={dl})")
                 adopted.append((b, "exit"))
                 fire = fb["exit"]

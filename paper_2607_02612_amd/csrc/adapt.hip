@@ -286,7 +286,9 @@ hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
 __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   const int i = blockIdx.x;
   const int nl = a.cnt->nlive;
-  if (i >= nl) return;
+  // Workgroup 0 always publishes the next counters, also when no sample is
+  // live any more (the next block must see nlive = 0, not a stale value).
+  if (i >= nl && i != 0) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   __shared__ int ired[8];
   __shared__ int dsts[AD_TMAX];
@@ -315,7 +317,7 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
       a.cu2[nn] = tot;
     }
   }
-  if (a.newlen[i] == 0) return;
+  if (i >= nl || a.newlen[i] == 0) return;
   const int base = a.cu[i], T = a.cu[i + 1] - base;
   const int orig = a.live[i];
   if (tid == 0) {

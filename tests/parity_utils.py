@@ -1,6 +1,11 @@
 """Helpers shared by the GPU parity tests: run the HIP path through the C ABI
 and check every sample against the CPU oracle, letting the oracle follow the
-GPU only at decisions whose oracle margin is below 1e-3 (near ties)."""
+GPU only at decisions whose oracle margin is below 1e-3 (near ties).
+
+On the bf16 path the exit-rule margin and the logit tolerance are the
+literal 1e-3 / 2e-2, raised to 2.5x the noise floor of the rounding contract
+where that is larger: the oracle drifts that far from itself when only the
+accumulation order of its matrix products changes (noise_floor.json)."""
 from __future__ import annotations
 
 import json
@@ -18,8 +23,35 @@ def mode_of(cfg):
     return "fp32" if cfg["precision"] == "fp32" else "bf16emu"
 
 
-def logit_tol(cfg):
-    return 1e-4 if cfg["precision"] == "fp32" else 2e-2
+def noise_floor(name, rho=1.0):
+    """Oracle-vs-oracle drift under a change of summation order only
+    (written by tests/golden/make_noise_floor.py)."""
+    with open(os.path.join(GOLDEN, "noise_floor.json")) as f:
+        data = json.load(f)
+    for w in data["workloads"]:
+        if w["workload"] == name and w["rho"] == rho:
+            return w
+    raise KeyError((name, rho))
+
+
+# Safety factor over the measured noise floor of the bf16 contract.
+FLOOR_FACTOR = 2.5
+
+
+def logit_tol(cfg, rho=1.0):
+    """1e-4 on the fp32 path; on the bf16 path 2e-2, raised to 2.5x the
+    contract's own summation-order noise floor where that is larger."""
+    if cfg["precision"] == "fp32":
+        return 1e-4
+    return max(2e-2, FLOOR_FACTOR * noise_floor(cfg["name"], rho)["max_dlogit"])
+
+
+def exit_tol(cfg, rho=1.0):
+    """Exit-rule margin (units of c) below which the two paths may disagree:
+    1e-3, raised to 2.5x the measured noise floor of c on the bf16 path."""
+    if cfg["precision"] == "fp32":
+        return 1e-3
+    return max(1e-3, FLOOR_FACTOR * noise_floor(cfg["name"], rho)["max_dc"])
 
 
 def exit_thresholds(name, rho):
@@ -28,6 +60,15 @@ def exit_thresholds(name, rho):
     for w in data["workloads"]:
         if w["workload"] == name and w["rho"] == rho:
             return {float(k): v for k, v in w["thresholds"].items()}
+    raise KeyError((name, rho))
+
+
+def exit_calibration(name, rho):
+    with open(os.path.join(GOLDEN, "exit_thresholds.json")) as f:
+        data = json.load(f)
+    for w in data["workloads"]:
+        if w["workload"] == name and w["rho"] == rho:
+            return w
     raise KeyError((name, rho))
 
 
@@ -84,11 +125,13 @@ def check_samples(cfg, W, imgs, res, idx, delta=None, rho=1.0):
     logits; returns (max |dlogit|, adopted near-tie decisions, details)."""
     mode = mode_of(cfg)
     Wp = fo.prepare_weights(W, mode)
-    tol = logit_tol(cfg)
+    tol = logit_tol(cfg, rho)
+    etol = exit_tol(cfg, rho)
     worst, adopted = 0.0, []
     for i in idx:
         out = fo.run_sample(imgs[i], Wp, cfg, mode, delta=delta, rho=rho,
-                            follow=follow_of(cfg, res, i))
+                            follow=follow_of(cfg, res, i),
+                            tol={"exit": etol, "other": fo.TOL})
         assert out["exit_block"] == res["exit_block"][i], i
         assert np.array_equal(out["token_counts"], res["counts"][i]), (
             i, out["token_counts"], res["counts"][i])
@@ -101,5 +144,5 @@ def check_samples(cfg, W, imgs, res, idx, delta=None, rho=1.0):
             if "m" in tb:
                 assert abs(tb["m"] - tr["m"][b - 1, i]) < 1e-4, (i, b)
             if "c" in tb:
-                assert abs(tb["c"] - tr["c"][b - 1, i]) < 2e-3, (i, b, tb["c"], tr["c"][b - 1, i])
+                assert abs(tb["c"] - tr["c"][b - 1, i]) < etol, (i, b, tb["c"], tr["c"][b - 1, i])
     return worst, adopted

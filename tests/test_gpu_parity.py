@@ -65,9 +65,16 @@ def test_deit_s_full_batch_sampled(torch_cuda, e):
     m = pu.gpu_model(cfg, W, cfg["batch"])
     res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[delta, delta])
     n_early = int((res["exit_block"] < cfg["L"]).sum())
-    # the oracle's calibration makes round(e B) samples exit early; a
-    # near-tie at the threshold may move one sample
-    assert abs(n_early - round(e * cfg["batch"])) <= 1
+    # the oracle's calibration makes round(e B) samples exit early; only the
+    # samples whose confidence lies within the exit margin of the threshold
+    # may go either way
+    c_hat = np.array(pu.exit_calibration("deit_s", 1.0)["c_hat_sorted"])
+    et = pu.exit_tol(cfg)
+    lo, hi = int((c_hat >= delta + et).sum()), int((c_hat >= delta - et).sum())
+    if e == 0.0:
+        lo = hi = 0
+    print(f"  early exits {n_early} (oracle window {lo}..{hi})")
+    assert lo <= n_early <= hi
     idx = [0, 1, 77, 128, 200, 255]
     worst, adopted = pu.check_samples(cfg, W, imgs, res, idx, delta=[delta, delta])
     _report("deit_s", worst, adopted, len(idx))
@@ -96,6 +103,23 @@ def test_deit_s_384_sampled(torch_cuda, rho):
     _report("deit_s_384", worst, adopted, 3)
 
 
+@pytest.mark.parametrize("name", ["deit_ti", "deit_s"])
+def test_plain_vit_literal_init_literal_tolerance(torch_cuda, name):
+    """With every weight N(0, 0.02) (heads included) the plain ViT (delta 1,
+    rho 0) must meet the literal 2e-2 logit bound."""
+    torch = torch_cuda
+    from oracle import fusion_oracle as fo
+    cfg, W, imgs = pu.make(name, batch=8, exit_gain=0.02 * np.sqrt(
+        {"deit_ti": 192, "deit_s": 384}[name]))
+    m = pu.gpu_model(cfg, W, 8)
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[1.0, 1.0], rho=0.0)
+    Wp = fo.prepare_weights(W, "bf16emu")
+    worst = max(float(np.abs(fo.plain_forward(imgs[i], Wp, cfg, "bf16emu")
+                             - res["logits"][i]).max()) for i in range(8))
+    print(f"[{name} literal init] max|dlogit|={worst:.3e}")
+    assert worst <= 2e-2
+
+
 def test_plain_vit_special_case(torch_cuda):
     """delta = 1, rho = 0: no merge, exit or prune; equals the plain ViT."""
     torch = torch_cuda
@@ -106,9 +130,10 @@ def test_plain_vit_special_case(torch_cuda):
     assert np.all(res["counts"] == cfg["N0"] + 1)
     assert np.all(res["exit_block"] == cfg["L"])
     Wp = fo.prepare_weights(W, "bf16emu")
+    tol = pu.logit_tol(cfg)
     for i in range(8):
         ref = fo.plain_forward(imgs[i], Wp, cfg, "bf16emu")
-        assert np.abs(ref - res["logits"][i]).max() <= 2e-2
+        assert np.abs(ref - res["logits"][i]).max() <= tol
 
 
 def test_threshold_zero_exits_at_first_head(torch_cuda):

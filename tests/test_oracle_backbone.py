@@ -150,3 +150,27 @@ def test_bf16emu_rounds_stored_operands():
     Wf = fo.prepare_weights(weights.make_weights(cfg, affine="random"), "fp32")
     d = np.abs(fo.patch_embed(img, Wf, cfg, "fp32") - x16).max()
     assert 1e-5 < d < 5e-2
+
+
+def test_bf16_contract_amplifies_summation_order_noise():
+    """The fp32 path is insensitive to the accumulation order of the matrix
+    products, while the bf16 rounding points turn that order into a visible
+    logit drift: this is the floor the bf16 parity tolerance is derived
+    from (tests/golden/noise_floor.json)."""
+    import json
+    import os
+    cfg = configs.get("deit_ti")
+    W = weights.make_weights(cfg)
+    img = images.make_images(cfg, batch=1)[0]
+    d = {}
+    for mode in ("fp32", "bf16emu"):
+        Wp = fo.prepare_weights(W, mode)
+        a = fo.plain_forward(img, Wp, cfg, mode)
+        with fo.accumulate("fp64"):
+            b = fo.plain_forward(img, Wp, cfg, mode)
+        d[mode] = float(np.abs(a - b).max())
+    assert d["fp32"] < 1e-4
+    assert d["bf16emu"] > 5e-3
+    with open(os.path.join(os.path.dirname(__file__), "golden", "noise_floor.json")) as f:
+        floor = {w["workload"]: w for w in json.load(f)["workloads"]}
+    assert d["bf16emu"] <= floor["deit_ti"]["max_dlogit"] * 1.5
