@@ -7,9 +7,10 @@
 // stored probabilities E are rounded to the storage type before they
 // multiply V, and O = (round(E) V) / l.
 //
-// One workgroup per (live sample, head); each of the 4 waves takes every
-// 4th query row.  K and V of the (sample, head) are staged in LDS when they
-// fit in 64 KB, else read from global memory.
+// bf16 path with 64-wide heads: MFMA kernel below.  fp32 path (and any
+// other head width): one workgroup per (live sample, head); each of the 4
+// waves takes every 4th query row; K and V of the (sample, head) are staged
+// in LDS when they fit in 64 KB, else read from global memory.
 #include "kernels.h"
 
 namespace fusion {
@@ -108,9 +109,209 @@ __global__ __launch_bounds__(256) void attention_valu(AttnArgs a) {
   }
 }
 
+// ------------------------------------------------------------ bf16 MFMA --
+// One workgroup per (live sample, head, block of 64 queries); each wave owns
+// 16 queries.  Scores are computed transposed, S^T = K Q^T, with
+// v_mfma_f32_16x16x32_bf16 so that every lane holds the scores of ONE query
+// (column l%16 of the output tile) for keys 16t + 4(l/16) + j: the exact row
+// maximum and the row sum are reductions over the lane's registers plus two
+// xor-shuffles (lanes l, l^16, l^32, l^48 share a query).  Keys are streamed
+// through LDS in chunks of 64 (K row-major; V transposed to [dh][key]), so
+// any length up to 16 * MAXT keys fits.  For O = P V the lane's own
+// probabilities of key tiles 2p and 2p+1 form the MFMA A operand directly:
+// the 8 k-slots of lane l map to keys {32p + 4g + i, 32p + 16 + 4g + i}
+// (g = l/16, i < 4), and the V operand is read from the transposed chunk
+// with the same key permutation (two 8-byte reads).
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int AKC = 64;            // keys per LDS chunk
+constexpr int AKS = 64 + 8;        // K chunk row stride (bf16), dh = 64
+constexpr int AVS = AKC + 8;       // V^T chunk row stride (bf16)
+
+template <int MAXT>
+__global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
+  const int i = blockIdx.x, h = blockIdx.y, qb = blockIdx.z;
+  if (i >= a.cnt->nlive) return;
+  const int base = a.cu[i], Tn = a.cu[i + 1] - base;
+  if (Tn > a.T_ub || Tn > 16 * MAXT) return;  // the host bound is exact
+  if (qb * 64 >= Tn) return;
+  if (h == 0 && qb == 0 && threadIdx.x == 0 && a.token_counts)
+    a.token_counts[a.live[i] * a.L + a.b0] = Tn;
+  const int d = a.d, ld = 3 * d;
+  const bf16_t* qkv = (const bf16_t*)a.qkv;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[AKC * AKS];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[64 * AVS];
+  __shared__ float lnS[16 * MAXT];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, c = lane & 15;
+  const int q0 = qb * 64 + wave * 16;   // first query of this wave
+  const int nkt = (Tn + 15) >> 4;       // key tiles
+  const int nch = (Tn + AKC - 1) / AKC; // key chunks
+
+  for (int j = tid; j < nkt * 16; j += 256)
+    lnS[j] = (j < Tn && a.prop_attn) ? logf(a.size[base + j]) : 0.f;
+
+  // Q^T operand: lane holds Q[q0 + c][8g .. 8g+7] and [32 + 8g ..]
+  bf16x8_t qop[2];
+  {
+    const int q = q0 + c;
+    const bf16_t* qr = qkv + (size_t)(base + q) * ld + h * 64;
+    for (int hf = 0; hf < 2; hf++) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (q < Tn) v = *(const uint4*)(qr + hf * 32 + 8 * g);
+      qop[hf] = *(bf16x8_t*)&v;
+    }
+  }
+
+  // ---- phase 1: S^T tiles for all keys
+  f32x4_t S[MAXT];
+#pragma unroll
+  for (int t = 0; t < MAXT; t++) S[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
+  for (int ch = 0; ch < nch; ch++) {
+    __syncthreads();
+    // stage 64 keys x 64 dims (rows beyond T are zero)
+    for (int u = tid; u < AKC * 8; u += 256) {
+      const int r = u >> 3, cc = (u & 7) * 8;
+      const int key = ch * AKC + r;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (key < Tn) v = *(const uint4*)(kg + (size_t)key * ld + cc);
+      *(uint4*)(Ks + r * AKS + cc) = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < MAXT; t++) {
+      if ((t >> 2) == ch) {
+        const bf16_t* kr = Ks + ((t & 3) * 16 + c) * AKS + 8 * g;
+        const bf16x8_t k0 = *(const bf16x8_t*)kr;
+        const bf16x8_t k1 = *(const bf16x8_t*)(kr + 32);
+        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[0], S[t], 0, 0, 0);
+        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[1], S[t], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- softmax with the exact row maximum (lane's query = q0 + c)
+  float mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < MAXT; t++) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int key = t * 16 + 4 * g + j;
+      float v = -INFINITY;
+      if (t < nkt && key < Tn) {
+        v = S[t][j] * a.scale;
+        if (a.prop_attn) v = v + lnS[key];
+      }
+      S[t][j] = v;
+      mx = fmaxf(mx, v);
+    }
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  float ls = 0.f;
+#pragma unroll
+  for (int t = 0; t < MAXT; t++)
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const float e = (t < nkt) ? expf(S[t][j] - mx) : 0.f;
+      S[t][j] = e;
+      ls += e;
+    }
+  ls += __shfl_xor(ls, 16, 64);
+  ls += __shfl_xor(ls, 32, 64);
+
+  if (a.cls_scores && q0 == 0 && c == 0) {
+    float* cs = a.cls_scores + ((size_t)i * a.H + h) * a.tmax;
+#pragma unroll
+    for (int t = 0; t < MAXT; t++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int key = t * 16 + 4 * g + j;
+        if (t < nkt && key < Tn) cs[key] = S[t][j] / ls;
+      }
+  }
+
+  // ---- phase 2: O = round(E) V over key-tile pairs
+  f32x4_t O[4];
+#pragma unroll
+  for (int n = 0; n < 4; n++) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
+  for (int ch = 0; ch < nch; ch++) {
+    __syncthreads();
+    // stage V^T for 64 keys: Vt[dim][key]; keys beyond T are zero
+    for (int u = tid; u < AKC * 8; u += 256) {
+      const int r = u >> 3, cc = (u & 7) * 8;
+      const int key = ch * AKC + r;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (key < Tn) v = *(const uint4*)(vg + (size_t)key * ld + cc);
+      const bf16_t* e = (const bf16_t*)&v;
+#pragma unroll
+      for (int q = 0; q < 8; q++) Vt[(cc + q) * AVS + r] = e[q];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < (MAXT + 1) / 2; p++) {
+      if ((p >> 1) == ch) {
+        const int t0 = 2 * p, t1 = 2 * p + 1;
+        bf16x8_t pa;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          pa[j] = (__bf16)0.f;
+          pa[4 + j] = (__bf16)0.f;
+        }
+        {
+          union { bf16_t u[8]; bf16x8_t v; } cv;
+#pragma unroll
+          for (int j = 0; j < 4; j++) {
+            cv.u[j] = f32_to_bf16(t0 < MAXT ? S[t0 < MAXT ? t0 : 0][j] : 0.f);
+            cv.u[4 + j] = f32_to_bf16(t1 < MAXT ? S[t1 < MAXT ? t1 : 0][j] : 0.f);
+          }
+          pa = cv.v;
+        }
+        const int kl = (p & 1) * 32 + 4 * g;  // key offset inside the chunk
+#pragma unroll
+        for (int n = 0; n < 4; n++) {
+          const bf16_t* vr = Vt + (n * 16 + c) * AVS + kl;
+          union { uint2 u[2]; bf16x8_t v; } vb;
+          vb.u[0] = *(const uint2*)vr;
+          vb.u[1] = *(const uint2*)(vr + 16);
+          O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb.v, O[n], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // ---- normalise and store: lane holds O[q0 + 4g + j][16n + c]
+  bf16_t* out = (bf16_t*)a.out;
+#pragma unroll
+  for (int j = 0; j < 4; j++) {
+    const int q = q0 + 4 * g + j;
+    const float l = __shfl(ls, 4 * g + j, 64);
+    if (q < Tn) {
+#pragma unroll
+      for (int n = 0; n < 4; n++)
+        out[(size_t)(base + q) * d + h * 64 + n * 16 + c] = f32_to_bf16(O[n][j] / l);
+    }
+  }
+}
+
 template <typename T>
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
+  if (sizeof(T) == 2 && a.dh == 64) {
+    dim3 grid(a.nlive_ub, a.H, (a.T_ub + 63) / 64);
+    if (a.T_ub <= 16 * 13)
+      attention_mfma<13><<<grid, 256, 0, s>>>(a);
+    else if (a.T_ub <= 16 * 40)
+      attention_mfma<40><<<grid, 256, 0, s>>>(a);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   const int ks = a.dh + (sizeof(T) == 2 ? 2 : 1);
   const size_t tail = (size_t)a.T_ub * 4 * 5 + (size_t)4 * a.dh * 4;
   const size_t staged = (((size_t)a.T_ub * ks * sizeof(T) + 15) & ~(size_t)15) +

@@ -28,10 +28,12 @@ def noise_floor(name, rho=1.0):
     (written by tests/golden/make_noise_floor.py)."""
     with open(os.path.join(GOLDEN, "noise_floor.json")) as f:
         data = json.load(f)
-    for w in data["workloads"]:
-        if w["workload"] == name and w["rho"] == rho:
+    rows = [w for w in data["workloads"] if w["workload"] == name]
+    for w in rows:
+        if w["rho"] == rho:
             return w
-    raise KeyError((name, rho))
+    # router strengths without their own measurement use the worst measured
+    return max(rows, key=lambda w: w["max_dlogit"])
 
 
 # Safety factor over the measured noise floor of the bf16 contract.
@@ -142,7 +144,8 @@ def check_samples(cfg, W, imgs, res, idx, delta=None, rho=1.0):
         tr = res["trace"]
         for b, tb in out["trace"].items():
             if "m" in tb:
-                assert abs(tb["m"] - tr["m"][b - 1, i]) < 1e-4, (i, b)
+                # router outputs agree within the router margin (units of m)
+                assert abs(tb["m"] - tr["m"][b - 1, i]) < (1e-5 if mode == "fp32" else fo.TOL), (i, b)
             if "c" in tb:
                 assert abs(tb["c"] - tr["c"][b - 1, i]) < etol, (i, b, tb["c"], tr["c"][b - 1, i])
     return worst, adopted
