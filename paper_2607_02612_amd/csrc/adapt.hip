@@ -5,18 +5,24 @@
 // followed by a separate compaction kernel that re-packs the surviving
 // samples and tokens (exclusive scans over new lengths and keep flags).
 //
-// One 256-thread workgroup per live sample.  No float atomics: every
-// reduction has a fixed order, so results do not depend on scheduling or on
-// the rest of the batch.
+// One 512-thread workgroup per live sample (the compaction uses 256).  No
+// float atomics: every reduction has a fixed order, so results do not depend
+// on scheduling or on the rest of the batch.
 #include "kernels.h"
 
 namespace fusion {
 
 constexpr int AD_TMAX = 640;  // tokens per sample (CLS included)
 constexpr int AD_AMAX = 320;  // |A| = ceil(N/2)
-constexpr int KC = 16;        // feature chunk of the similarity tiles
-constexpr int AG = 64;        // A rows per similarity pass
-constexpr int BG = 128;       // B rows per similarity pass
+constexpr int AD_BMAX = 320;  // |B| = floor(N/2)
+constexpr int AD_NT = 512;    // threads per workgroup (8 waves)
+constexpr int SKC = 32;       // feature chunk of the similarity MFMAs
+constexpr int SKP = SKC + 8;  // padded LDS row (bf16)
+constexpr int SAG = 128;      // A rows per pass: one 16-row MFMA tile per wave
+constexpr int SNBT = AD_BMAX / 16;  // B tiles held in registers
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ int merge_count(float m, double rho, int r_b, int N) {
   // r = clamp(floor(((2 rho) m) r_b + 1/2), 0, floor(N/2)), every step an
@@ -29,7 +35,146 @@ __device__ __forceinline__ int merge_count(float m, double rho, int r_b, int N) 
   return r;
 }
 
-__global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
+// Block-wide reductions for AD_NT threads (8 waves); red >= 8 entries.
+__device__ __forceinline__ float bsum(float v, float* red) {
+  v = wave_sum(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int w = 0; w < AD_NT / 64; w++) s += red[w];
+  return s;
+}
+__device__ __forceinline__ float bmax(float v, float* red) {
+  v = wave_max(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float s = red[0];
+#pragma unroll
+  for (int w = 1; w < AD_NT / 64; w++) s = fmaxf(s, red[w]);
+  return s;
+}
+__device__ __forceinline__ int bsum_i(int v, int* red) {
+  v = wave_sum_i(v);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int s = 0;
+#pragma unroll
+  for (int w = 0; w < AD_NT / 64; w++) s += red[w];
+  return s;
+}
+
+// Split a float into bf16 hi + lo with hi + lo = v to about 2^-17 relative.
+__device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
+  hi = f32_to_bf16(v);
+  lo = f32_to_bf16(v - bf16_to_f32(hi));
+}
+
+// Cosine similarities of the A tokens (even patch slots) with the B tokens
+// (odd slots) of one sample, and the best B for every A.  The features are
+// the fp32 hidden states divided by their clamped norms; each is split into
+// bf16 hi + lo and the dot products take hi.hi' + hi.lo' + lo.hi' on
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation (absolute error of a
+// cosine <= ~1.2e-5, the dropped lo.lo' term included).  Wave w owns A rows
+// ag + 16w .. +15 against every B tile; lane l of an output tile holds
+// S[a = 4(l/16) + j][b = l%16].
+__device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
+                                  int nA, int nB, const float* nrm,
+                                  float* bestsim, int* best, bf16_t* Ahi,
+                                  bf16_t* Alo, bf16_t* Bhi, bf16_t* Blo) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, c = lane & 15;
+  const int nbt = (nB + 15) >> 4;
+  for (int ag = 0; ag < nA; ag += SAG) {
+    f32x4_t acc[SNBT];
+#pragma unroll
+    for (int t = 0; t < SNBT; t++) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < d; k0 += SKC) {
+      __syncthreads();
+      // stage normalised features as hi/lo bf16 (rows beyond the sets are 0)
+      for (int u = tid; u < (SAG + nbt * 16) * (SKC / 4); u += AD_NT) {
+        const int r = u / (SKC / 4), q = (u - r * (SKC / 4)) * 4;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        float inv = 0.f;
+        bf16_t* H;
+        bf16_t* Lo;
+        int rr;
+        if (r < SAG) {
+          const int aa = ag + r;
+          rr = r;
+          H = Ahi;
+          Lo = Alo;
+          if (aa < nA) {
+            v = *(const float4*)(x + (size_t)(base + 1 + 2 * aa) * d + k0 + q);
+            inv = nrm[2 * aa];
+          }
+        } else {
+          const int bb = r - SAG;
+          rr = bb;
+          H = Bhi;
+          Lo = Blo;
+          if (bb < nB) {
+            v = *(const float4*)(x + (size_t)(base + 2 + 2 * bb) * d + k0 + q);
+            inv = nrm[2 * bb + 1];
+          }
+        }
+        const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int z = 0; z < 4; z++) {
+          const float f = inv > 0.f ? e[z] / inv : 0.f;
+          split_bf16(f, H[rr * SKP + q + z], Lo[rr * SKP + q + z]);
+        }
+      }
+      __syncthreads();
+      const bf16x8_t ah = *(const bf16x8_t*)(Ahi + (wave * 16 + c) * SKP + 8 * g);
+      const bf16x8_t al = *(const bf16x8_t*)(Alo + (wave * 16 + c) * SKP + 8 * g);
+#pragma unroll
+      for (int t = 0; t < SNBT; t++) {
+        if (t < nbt) {
+          const bf16x8_t bh = *(const bf16x8_t*)(Bhi + (t * 16 + c) * SKP + 8 * g);
+          const bf16x8_t bl = *(const bf16x8_t*)(Blo + (t * 16 + c) * SKP + 8 * g);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc[t], 0, 0, 0);
+          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc[t], 0, 0, 0);
+        }
+      }
+    }
+    // argmax over B for the lane's 4 A rows, ties to the lowest B index
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      float bv = -INFINITY;
+      int bi = 0x7fffffff;
+#pragma unroll
+      for (int t = 0; t < SNBT; t++) {
+        const int bb = t * 16 + c;
+        if (t < nbt && bb < nB && acc[t][j] > bv) {
+          bv = acc[t][j];
+          bi = bb;
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ov > bv || (ov == bv && oi < bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      const int aa = ag + wave * 16 + 4 * g + j;
+      if (c == 0 && aa < nA) {
+        bestsim[aa] = bv;
+        best[aa] = bi < nB ? bi : 0;  // bi >= nB only with non-finite x
+      }
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   const int i = blockIdx.x;
   if (i >= a.cnt->nlive) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -45,18 +190,18 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
   __shared__ int best[AD_AMAX];
   __shared__ int chosen[AD_AMAX];
   __shared__ int clist[AD_AMAX];
-  __shared__ float tmpf[AD_AMAX];
-  __shared__ float tmps[AD_AMAX];
-  __shared__ float xa[AG][KC + 1];
-  __shared__ float xb[BG][KC + 1];
-  __shared__ float rbv[16][AG];
-  __shared__ int rbi[16][AG];
-  __shared__ float red[8];
-  __shared__ int ired[8];
+  __shared__ float tmpf[AD_BMAX];
+  __shared__ float tmps[AD_BMAX];
+  __shared__ __attribute__((aligned(16))) bf16_t Ahi[SAG * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Alo[SAG * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bhi[AD_BMAX * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Blo[AD_BMAX * SKP];
+  __shared__ float red[16];
+  __shared__ int ired[16];
 
-  for (int t = tid; t < T; t += 256) keepf[t] = 1;
+  for (int t = tid; t < T; t += AD_NT) keepf[t] = 1;
   if (a.isP) {
-    for (int t = tid; t < T; t += 256) {
+    for (int t = tid; t < T; t += AD_NT) {
       float s = a.cls_scores[((size_t)i * a.H) * a.tmax + t];
       for (int h = 1; h < a.H; h++) s = s + a.cls_scores[((size_t)i * a.H + h) * a.tmax + t];
       sc[t] = s / (float)a.H;
@@ -68,8 +213,8 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
   int r = 0;
   if (a.isM) {
     float z = 0.f;
-    for (int k = tid; k < d; k += 256) z = fmaf(a.router_w[k], a.x[(size_t)base * d + k], z);
-    z = block_sum256(z, red) + a.router_b[0];
+    for (int k = tid; k < d; k += AD_NT) z = fmaf(a.router_w[k], a.x[(size_t)base * d + k], z);
+    z = bsum(z, red) + a.router_b[0];
     const float m = 1.0f / (1.0f + expf(-z));
     r = merge_count(m, a.rho, a.r_b, N);
     if (tid == 0) {
@@ -80,7 +225,7 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
   const int nA = (N + 1) / 2, nB = N / 2;
   if (r > 0) {
     // clamped L2 norms of the patch tokens
-    for (int j = wave; j < N; j += 4) {
+    for (int j = wave; j < N; j += AD_NT / 64) {
       const float* xr = a.x + (size_t)(base + 1 + j) * d;
       float ss = 0.f;
       for (int k = lane; k < d; k += 64) ss = fmaf(xr[k], xr[k], ss);
@@ -88,75 +233,9 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
       if (lane == 0) nrm[j] = fmaxf(sqrtf(ss), 1e-12f);
     }
     __syncthreads();
-    // cosine similarities A x B in passes of AG x BG; running argmax per A
-    const int ta = tid & 15, tb = tid >> 4;
-    for (int ag = 0; ag < nA; ag += AG) {
-      for (int bg = 0; bg < nB; bg += BG) {
-        float acc[4][8];
-#pragma unroll
-        for (int q = 0; q < 4; q++)
-#pragma unroll
-          for (int jj = 0; jj < 8; jj++) acc[q][jj] = 0.f;
-        for (int k0 = 0; k0 < d; k0 += KC) {
-          for (int idx = tid; idx < AG * KC; idx += 256) {
-            const int rr = idx / KC, kk = idx - rr * KC, aa = ag + rr;
-            xa[rr][kk] = aa < nA ? a.x[(size_t)(base + 1 + 2 * aa) * d + k0 + kk] / nrm[2 * aa] : 0.f;
-          }
-          for (int idx = tid; idx < BG * KC; idx += 256) {
-            const int rr = idx / KC, kk = idx - rr * KC, bb = bg + rr;
-            xb[rr][kk] = bb < nB ? a.x[(size_t)(base + 2 + 2 * bb) * d + k0 + kk] / nrm[2 * bb + 1] : 0.f;
-          }
-          __syncthreads();
-#pragma unroll
-          for (int kk = 0; kk < KC; kk++) {
-            float av[4], bv[8];
-#pragma unroll
-            for (int q = 0; q < 4; q++) av[q] = xa[ta * 4 + q][kk];
-#pragma unroll
-            for (int jj = 0; jj < 8; jj++) bv[jj] = xb[tb + 16 * jj][kk];
-#pragma unroll
-            for (int q = 0; q < 4; q++)
-#pragma unroll
-              for (int jj = 0; jj < 8; jj++) acc[q][jj] = fmaf(av[q], bv[jj], acc[q][jj]);
-          }
-          __syncthreads();
-        }
-#pragma unroll
-        for (int q = 0; q < 4; q++) {
-          float bvv = -INFINITY;
-          int bi = 0x7fffffff;
-#pragma unroll
-          for (int jj = 0; jj < 8; jj++) {
-            const int bb = bg + tb + 16 * jj;
-            if (bb < nB && acc[q][jj] > bvv) {
-              bvv = acc[q][jj];
-              bi = bb;
-            }
-          }
-          rbv[tb][ta * 4 + q] = bvv;
-          rbi[tb][ta * 4 + q] = bi;
-        }
-        __syncthreads();
-        if (tid < AG && ag + tid < nA) {
-          const int aa = ag + tid;
-          float v = bg == 0 ? -INFINITY : bestsim[aa];
-          int vi = bg == 0 ? 0x7fffffff : best[aa];
-          for (int t = 0; t < 16; t++) {
-            const float cv = rbv[t][tid];
-            const int ci = rbi[t][tid];
-            if (cv > v || (cv == v && ci < vi)) {
-              v = cv;
-              vi = ci;
-            }
-          }
-          bestsim[aa] = v;
-          best[aa] = vi < nB ? vi : 0;  // only reachable with non-finite x
-        }
-        __syncthreads();
-      }
-    }
+    similarity_argmax(a.x, base, d, nA, nB, nrm, bestsim, best, Ahi, Alo, Bhi, Blo);
     // top-r of A by best similarity, ties to the lower A slot
-    for (int aa = tid; aa < nA; aa += 256) {
+    for (int aa = tid; aa < nA; aa += AD_NT) {
       const float v = bestsim[aa];
       int rank = 0;
       for (int a2 = 0; a2 < nA; a2++) {
@@ -173,7 +252,7 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
     }
     __syncthreads();
     // size-weighted merge into each destination, sources in ascending order
-    for (int idx = tid; idx < nB * d; idx += 256) {
+    for (int idx = tid; idx < nB * d; idx += AD_NT) {
       const int bb = idx / d, f = idx - bb * d;
       const size_t rowb = (size_t)(base + 2 + 2 * bb);
       float num = a.size[rowb] * a.x[rowb * d + f];
@@ -190,7 +269,7 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
       }
       if (has) a.x[rowb * d + f] = num / den;
     }
-    for (int bb = tid; bb < nB; bb += 256) {
+    for (int bb = tid; bb < nB; bb += AD_NT) {
       float den = a.size[base + 2 + 2 * bb];
       float s2 = a.isP ? sc[2 + 2 * bb] : 0.f;
       for (int q = 0; q < r; q++) {
@@ -204,11 +283,11 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
       tmps[bb] = s2;
     }
     __syncthreads();
-    for (int bb = tid; bb < nB; bb += 256) {
+    for (int bb = tid; bb < nB; bb += AD_NT) {
       a.size[base + 2 + 2 * bb] = tmpf[bb];
       if (a.isP) sc[2 + 2 * bb] = tmps[bb];
     }
-    for (int q = tid; q < r; q += 256) {
+    for (int q = tid; q < r; q += AD_NT) {
       const int aa = clist[q];
       keepf[1 + 2 * aa] = 0;
       if (a.tr_merge)
@@ -223,16 +302,16 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
   if (a.isE) {
     const float* lg = a.head_buf + (size_t)i * a.C;
     float lm = -INFINITY;
-    for (int k = tid; k < a.C; k += 256) lm = fmaxf(lm, lg[k]);
-    lm = block_max256(lm, red);
+    for (int k = tid; k < a.C; k += AD_NT) lm = fmaxf(lm, lg[k]);
+    lm = bmax(lm, red);
     float s = 0.f;
-    for (int k = tid; k < a.C; k += 256) s += expf(lg[k] - lm);
-    s = block_sum256(s, red);
+    for (int k = tid; k < a.C; k += AD_NT) s += expf(lg[k] - lm);
+    s = bsum(s, red);
     const float c = 1.0f / s;
     fire = (a.delta < 1.0f) && (c >= a.delta);
     if (tid == 0 && a.tr_c) a.tr_c[tr_row] = c;
     if (fire) {
-      for (int k = tid; k < a.C; k += 256) a.logits[(size_t)orig * a.C + k] = lg[k];
+      for (int k = tid; k < a.C; k += AD_NT) a.logits[(size_t)orig * a.C + k] = lg[k];
       if (tid == 0) a.exit_block[orig] = a.b;
     }
   }
@@ -240,13 +319,14 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
   // ----------------------------------------------------------- prune --
   if (a.isP && !fire) {
     int ns = 0;
-    for (int t = 1 + tid; t < T; t += 256) ns += keepf[t];
-    ns = block_sum256_i(ns, ired);
+    for (int t = 1 + tid; t < T; t += AD_NT) ns += keepf[t];
+    ns = bsum_i(ns, ired);
     const int k = (int)floor(__dmul_rn(a.tau_eff, (double)ns));
-    int keep_new[(AD_TMAX + 255) / 256];
+    constexpr int U = (AD_TMAX + AD_NT - 1) / AD_NT;
+    int keep_new[U];
 #pragma unroll
-    for (int u = 0; u < (AD_TMAX + 255) / 256; u++) {
-      const int t = 1 + tid + u * 256;
+    for (int u = 0; u < U; u++) {
+      const int t = 1 + tid + u * AD_NT;
       keep_new[u] = 0;
       if (t < T && keepf[t]) {
         const float v = sc[t];
@@ -258,27 +338,27 @@ __global__ __launch_bounds__(256) void adapt_kernel(AdaptArgs a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < (AD_TMAX + 255) / 256; u++) {
-      const int t = 1 + tid + u * 256;
+    for (int u = 0; u < U; u++) {
+      const int t = 1 + tid + u * AD_NT;
       if (t < T) keepf[t] = keep_new[u];
     }
     __syncthreads();
   }
 
   int cnt = 0;
-  for (int t = tid; t < T; t += 256) {
+  for (int t = tid; t < T; t += AD_NT) {
     const int kf = fire ? 0 : keepf[t];
     a.keep[base + t] = kf;
     cnt += kf;
   }
-  cnt = block_sum256_i(cnt, ired);
+  cnt = bsum_i(cnt, ired);
   if (tid == 0) a.newlen[i] = cnt;
 }
 
 hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
-  if (a.n0 + 1 > AD_TMAX || a.d % KC != 0) return hipErrorInvalidValue;
-  adapt_kernel<<<a.nlive_ub, 256, 0, s>>>(a);
+  if (a.n0 + 1 > AD_TMAX || a.d % SKC != 0) return hipErrorInvalidValue;
+  adapt_kernel<<<a.nlive_ub, AD_NT, 0, s>>>(a);
   return hipGetLastError();
 }
 

@@ -99,23 +99,37 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 
 // ------------------------------------------------------------ bf16 MFMA --
 // 256 threads = 4 waves in a 2x2 grid; each wave owns a 64x64 sub-tile made
-// of 2x2 MFMA 32x32 blocks.  A and W tiles are [128][BK] bf16 in LDS with a
-// padded row stride (BK + 8) so that the 16-byte per-lane operand reads of
-// consecutive rows fall in different banks.
+// of 2x2 MFMA 32x32 blocks.  A and W tiles are [128][KB] bf16 in LDS with a
+// padded row stride (KB + 8) so that the 16-byte per-lane operand reads of
+// consecutive rows fall in different banks.  The K loop is software
+// pipelined: the global loads of tile k+1 are issued into registers before
+// the MFMAs of tile k, and the LDS is double buffered, so one barrier per K
+// step separates the producer and consumer halves.
+//
+// Tile order: blocks are dispatched round-robin over the 8 XCDs (block id %
+// 8).  The linear block id is remapped so that every XCD walks whole row
+// panels (all N tiles of one M tile back to back): the A panel is fetched
+// into that XCD's L2 once and reused by all its N tiles.
 //
 // Operand layout of v_mfma_f32_32x32x16_bf16 (64 lanes): lane l supplies
 // A[row l%32][k 8*(l/32) .. +7] and B[k 8*(l/32) .. +7][col l%32]; result
 // element q of lane l is C[8*(q/4) + 4*(l/32) + q%4][l%32].
 constexpr int MB = 128, NB = 128, KB = 64, KP = KB + 8;
+constexpr int NXCD = 8;
 
-__global__ __launch_bounds__(256) void gemm_mfma_bf16(
+__global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
-    int N, int K, const int* M_dev, int M_host, Epi e) {
+    int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
   const int M = M_dev ? *M_dev : M_host;
-  const int m0 = blockIdx.x * MB, n0 = blockIdx.y * NB;
-  if (m0 >= M) return;
-  __shared__ __attribute__((aligned(16))) bf16_t As[MB * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[NB * KP];
+  const int n_nt = (N + NB - 1) / NB;
+  // XCD-aware remap of the 1-D grid (size = round_up(n_mt, 8) * n_nt)
+  const int id = blockIdx.x;
+  const int xcd = id % NXCD, local = id / NXCD;
+  const int mt = (local / n_nt) * NXCD + xcd, nt = local % n_nt;
+  const int m0 = mt * MB, n0 = nt * NB;
+  if (mt >= n_mt || m0 >= M) return;
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][MB * KP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][NB * KP];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   f32x16_t acc[2][2];
@@ -126,34 +140,52 @@ __global__ __launch_bounds__(256) void gemm_mfma_bf16(
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[i][j][q] = 0.f;
 
-  for (int k0 = 0; k0 < K; k0 += KB) {
+  // each thread moves 4 16-byte chunks of A and of W per K tile
+  uint4 ra[4], rb[4];
+  auto gload = [&](int k0) {
 #pragma unroll
     for (int c = 0; c < 4; c++) {
       const int chunk = tid + c * 256;
       const int r = chunk >> 3, kc = (chunk & 7) * 8;
-      uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
-      if (m0 + r < M) va = *(const uint4*)(A + (size_t)(m0 + r) * lda + k0 + kc);
-      if (n0 + r < N) vb = *(const uint4*)(W + (size_t)(n0 + r) * K + k0 + kc);
-      *(uint4*)(As + r * KP + kc) = va;
-      *(uint4*)(Bs + r * KP + kc) = vb;
+      ra[c] = make_uint4(0, 0, 0, 0);
+      rb[c] = make_uint4(0, 0, 0, 0);
+      if (m0 + r < M) ra[c] = *(const uint4*)(A + (size_t)(m0 + r) * lda + k0 + kc);
+      if (n0 + r < N) rb[c] = *(const uint4*)(W + (size_t)(n0 + r) * K + k0 + kc);
     }
-    __syncthreads();
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+      const int chunk = tid + c * 256;
+      const int r = chunk >> 3, kc = (chunk & 7) * 8;
+      *(uint4*)(As[buf] + r * KP + kc) = ra[c];
+      *(uint4*)(Bs[buf] + r * KP + kc) = rb[c];
+    }
+  };
+  const int nk = K / KB;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt++) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * KB);
 #pragma unroll
     for (int ks = 0; ks < KB; ks += 16) {
       bf16x8_t a[2], b[2];
       const int ko = ks + (lane >> 5) * 8;
 #pragma unroll
       for (int i = 0; i < 2; i++)
-        a[i] = *(const bf16x8_t*)(As + (wm * 64 + i * 32 + (lane & 31)) * KP + ko);
+        a[i] = *(const bf16x8_t*)(As[buf] + (wm * 64 + i * 32 + (lane & 31)) * KP + ko);
 #pragma unroll
       for (int j = 0; j < 2; j++)
-        b[j] = *(const bf16x8_t*)(Bs + (wn * 64 + j * 32 + (lane & 31)) * KP + ko);
+        b[j] = *(const bf16x8_t*)(Bs[buf] + (wn * 64 + j * 32 + (lane & 31)) * KP + ko);
 #pragma unroll
       for (int i = 0; i < 2; i++)
 #pragma unroll
         for (int j = 0; j < 2; j++)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+    if (kt + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
   }
 #pragma unroll
@@ -188,8 +220,9 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   // The MFMA tiles need K % 64 == 0 and 16-byte aligned rows; the model
   // creation rejects bf16 shapes that do not satisfy this.
   if (K % KB != 0 || lda % 8 != 0) return hipErrorInvalidValue;
-  dim3 grid((M_ub + MB - 1) / MB, (N + NB - 1) / NB);
-  gemm_mfma_bf16<<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, e);
+  const int n_mt = (M_ub + MB - 1) / MB, n_nt = (N + NB - 1) / NB;
+  const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
+  gemm_mfma_bf16<<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e);
   return hipGetLastError();
 }
 
