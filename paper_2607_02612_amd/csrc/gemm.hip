@@ -98,38 +98,56 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 }
 
 // ------------------------------------------------------------ bf16 MFMA --
-// 256 threads = 4 waves in a 2x2 grid; each wave owns a 64x64 sub-tile made
-// of 2x2 MFMA 32x32 blocks.  A and W tiles are [128][KB] bf16 in LDS with a
-// padded row stride (KB + 8) so that the 16-byte per-lane operand reads of
-// consecutive rows fall in different banks.  The K loop is software
-// pipelined: the global loads of tile k+1 are issued into registers before
-// the MFMAs of tile k, and the LDS is double buffered, so one barrier per K
-// step separates the producer and consumer halves.
+// 128x128 output tile per workgroup, 4 waves in a 2x2 grid, each wave a
+// 64x64 sub-tile of 2x2 v_mfma_f32_32x32x16_bf16 blocks.
+//
+// K is consumed in steps of 32.  A and W tiles reach LDS through the gfx950
+// asynchronous global->LDS path (global_load_lds_dwordx4): each wave-wide
+// instruction writes 64 lanes x 16 bytes contiguously, i.e. 16 rows of 64
+// bytes, without passing through VGPRs, so NSTG = 3 K steps are in flight
+// in a ring of LDS stages while the matrix cores work on the oldest one.
+// The loads are issued from inline assembly and their completion is awaited
+// with explicit vmcnt counts (a compiler-visible LDS DMA would make every
+// LDS read wait for all outstanding loads).  Rows are stored with their four
+// 16-byte chunks XOR-permuted by (row / 4) % 4, which makes the per-lane
+// 16-byte operand reads of 16 consecutive rows hit 16 disjoint bank groups.
+// Rows past M or N are clamped to the last valid row for the loads (every
+// address stays in bounds) and masked in the epilogue.
 //
 // Tile order: blocks are dispatched round-robin over the 8 XCDs (block id %
-// 8).  The linear block id is remapped so that every XCD walks whole row
-// panels (all N tiles of one M tile back to back): the A panel is fetched
-// into that XCD's L2 once and reused by all its N tiles.
+// 8); the linear id is remapped so that each XCD walks whole row panels (all
+// N tiles of one M tile back to back) and reuses the A panel in its own L2.
 //
 // Operand layout of v_mfma_f32_32x32x16_bf16 (64 lanes): lane l supplies
 // A[row l%32][k 8*(l/32) .. +7] and B[k 8*(l/32) .. +7][col l%32]; result
 // element q of lane l is C[8*(q/4) + 4*(l/32) + q%4][l%32].
-constexpr int MB = 128, NB = 128, KB = 64, KP = KB + 8;
+constexpr int MB = 128, NB = 128, KS = 32, NSTG = 3;
+constexpr int ROWB = KS * 2;                 // bytes per staged row
+constexpr int STGB = (MB + NB) * ROWB;       // bytes per stage
 constexpr int NXCD = 8;
+constexpr int DMA_PER_WAVE = (MB + NB) / 16 / 4;
 
-__global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(
+__device__ __forceinline__ void dma16(const void* gptr, unsigned lds_byte_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(gptr), "s"(lds_byte_addr) : "memory", "m0");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+__global__ __launch_bounds__(256) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
     int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
   const int M = M_dev ? *M_dev : M_host;
   const int n_nt = (N + NB - 1) / NB;
-  // XCD-aware remap of the 1-D grid (size = round_up(n_mt, 8) * n_nt)
   const int id = blockIdx.x;
   const int xcd = id % NXCD, local = id / NXCD;
   const int mt = (local / n_nt) * NXCD + xcd, nt = local % n_nt;
   const int m0 = mt * MB, n0 = nt * NB;
   if (mt >= n_mt || m0 >= M) return;
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][MB * KP];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][NB * KP];
+  __shared__ __attribute__((aligned(16))) char smem[NSTG * STGB];
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void*)smem;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   f32x16_t acc[2][2];
@@ -140,53 +158,70 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_bf16(
 #pragma unroll
       for (int q = 0; q < 16; q++) acc[i][j][q] = 0.f;
 
-  // each thread moves 4 16-byte chunks of A and of W per K tile
-  uint4 ra[4], rb[4];
-  auto gload = [&](int k0) {
+  // this lane's source row and LDS slot for each of the wave's DMA
+  // instructions (16-row blocks: A rows first, then W rows)
+  const bf16_t* src[DMA_PER_WAVE];
+  unsigned dst[DMA_PER_WAVE];
 #pragma unroll
-    for (int c = 0; c < 4; c++) {
-      const int chunk = tid + c * 256;
-      const int r = chunk >> 3, kc = (chunk & 7) * 8;
-      ra[c] = make_uint4(0, 0, 0, 0);
-      rb[c] = make_uint4(0, 0, 0, 0);
-      if (m0 + r < M) ra[c] = *(const uint4*)(A + (size_t)(m0 + r) * lda + k0 + kc);
-      if (n0 + r < N) rb[c] = *(const uint4*)(W + (size_t)(n0 + r) * K + k0 + kc);
+  for (int u = 0; u < DMA_PER_WAVE; u++) {
+    const int q = wave * DMA_PER_WAVE + u;
+    const bool isA = q < MB / 16;
+    const int r = (isA ? q : q - MB / 16) * 16 + (lane >> 2);
+    const int chunk = (lane & 3) ^ ((r >> 2) & 3);
+    if (isA) {
+      const int gr = min(m0 + r, M - 1);
+      src[u] = A + (size_t)gr * lda + chunk * 8;
+      dst[u] = q * 16 * ROWB;
+    } else {
+      const int gr = min(n0 + r, N - 1);
+      src[u] = W + (size_t)gr * K + chunk * 8;
+      dst[u] = MB * ROWB + (q - MB / 16) * 16 * ROWB;
     }
-  };
-  auto lstore = [&](int buf) {
+  }
+  const int nk = K / KS;
 #pragma unroll
-    for (int c = 0; c < 4; c++) {
-      const int chunk = tid + c * 256;
-      const int r = chunk >> 3, kc = (chunk & 7) * 8;
-      *(uint4*)(As[buf] + r * KP + kc) = ra[c];
-      *(uint4*)(Bs[buf] + r * KP + kc) = rb[c];
+  for (int st = 0; st < NSTG - 1; st++)
+    if (st < nk) {
+#pragma unroll
+      for (int u = 0; u < DMA_PER_WAVE; u++)
+        dma16(src[u] + st * KS, __builtin_amdgcn_readfirstlane(lds0 + st * STGB + dst[u]));
     }
-  };
-  const int nk = K / KB;
-  gload(0);
-  lstore(0);
-  __syncthreads();
   for (int kt = 0; kt < nk; kt++) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * KB);
+    // stage kt has landed once at most the later stages are outstanding
+    if (kt + 1 < nk)
+      wait_vm<DMA_PER_WAVE * (NSTG - 2)>();
+    else
+      wait_vm<0>();
+    __syncthreads();
+    const int kn = kt + NSTG - 1;
+    if (kn < nk) {
+      const unsigned sb = lds0 + (kn % NSTG) * STGB;
 #pragma unroll
-    for (int ks = 0; ks < KB; ks += 16) {
+      for (int u = 0; u < DMA_PER_WAVE; u++)
+        dma16(src[u] + kn * KS, __builtin_amdgcn_readfirstlane(sb + dst[u]));
+    }
+    const char* Ab = smem + (kt % NSTG) * STGB;
+    const char* Bb = Ab + MB * ROWB;
+#pragma unroll
+    for (int ks = 0; ks < KS; ks += 16) {
       bf16x8_t a[2], b[2];
-      const int ko = ks + (lane >> 5) * 8;
+      const int c = (ks >> 3) + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 2; i++)
-        a[i] = *(const bf16x8_t*)(As[buf] + (wm * 64 + i * 32 + (lane & 31)) * KP + ko);
+      for (int i = 0; i < 2; i++) {
+        const int r = wm * 64 + i * 32 + (lane & 31);
+        a[i] = *(const bf16x8_t*)(Ab + r * ROWB + ((c ^ ((r >> 2) & 3)) << 4));
+      }
 #pragma unroll
-      for (int j = 0; j < 2; j++)
-        b[j] = *(const bf16x8_t*)(Bs[buf] + (wn * 64 + j * 32 + (lane & 31)) * KP + ko);
+      for (int j = 0; j < 2; j++) {
+        const int r = wn * 64 + j * 32 + (lane & 31);
+        b[j] = *(const bf16x8_t*)(Bb + r * ROWB + ((c ^ ((r >> 2) & 3)) << 4));
+      }
 #pragma unroll
       for (int i = 0; i < 2; i++)
 #pragma unroll
         for (int j = 0; j < 2; j++)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
   }
 #pragma unroll
   for (int i = 0; i < 2; i++)
@@ -217,9 +252,9 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
                                int N, int K, const int* M_dev, int M_host,
                                int M_ub, const Epi& e, hipStream_t s) {
   if (M_ub <= 0) return hipSuccess;
-  // The MFMA tiles need K % 64 == 0 and 16-byte aligned rows; the model
+  // The K steps need K % 32 == 0 and 16-byte aligned rows; the model
   // creation rejects bf16 shapes that do not satisfy this.
-  if (K % KB != 0 || lda % 8 != 0) return hipErrorInvalidValue;
+  if (K % KS != 0 || lda % 8 != 0 || K <= 0) return hipErrorInvalidValue;
   const int n_mt = (M_ub + MB - 1) / MB, n_nt = (N + NB - 1) / NB;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
   gemm_mfma_bf16<<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e);

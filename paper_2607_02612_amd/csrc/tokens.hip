@@ -52,30 +52,35 @@ hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
 }
 
 // images [B, C, S, S] -> patches [B*n0, C*p*p]; patch (gy, gx) in raster
-// order, vector element (c, ky, kx).
+// order, vector element (c, ky, kx).  One work item copies the p contiguous
+// pixels of one (patch, channel, kernel row); index math in 32 bits (the
+// host checks that B * n0 * C * p fits).
 template <typename T>
 __global__ void patchify_kernel(const float* __restrict__ img, T* __restrict__ out,
                                 int B, int C, int S, int p) {
-  const int g = S / p, n0 = g * g, pd = C * p * p;
-  const long total = (long)B * n0 * pd;
-  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < total;
-       t += (long)gridDim.x * blockDim.x) {
-    const long row = t / pd;
-    const int e = (int)(t - row * pd);
-    const int s = (int)(row / n0), j = (int)(row - (long)s * n0);
+  const int g = S / p, n0 = g * g;
+  const int items = B * n0 * C * p;
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < items;
+       t += gridDim.x * blockDim.x) {
+    int rest = t;
+    const int ky = rest % p;
+    rest /= p;
+    const int c = rest % C;
+    const int row = rest / C;            // global patch row s * n0 + j
+    const int s = row / n0, j = row - s * n0;
     const int gy = j / g, gx = j - gy * g;
-    const int c = e / (p * p), rem = e - c * p * p;
-    const int ky = rem / p, kx = rem - ky * p;
-    const float v = img[(((size_t)s * C + c) * S + gy * p + ky) * S + gx * p + kx];
-    out[t] = St<T>::put(v);
+    const float* src = img + (((size_t)s * C + c) * S + gy * p + ky) * S + gx * p;
+    T* dst = out + (size_t)row * (C * p * p) + (c * p + ky) * p;
+    for (int kx = 0; kx < p; kx++) dst[kx] = St<T>::put(src[kx]);
   }
 }
 
 template <typename T>
 hipError_t launch_patchify(const float* img, T* out, int B, int C, int S,
                            int p, hipStream_t s) {
-  const long total = (long)B * (S / p) * (S / p) * C * p * p;
-  int blocks = (int)((total + 255) / 256);
+  const long items = (long)B * (S / p) * (S / p) * C * p;
+  if (items >= (1L << 31)) return hipErrorInvalidValue;
+  int blocks = (int)((items + 255) / 256);
   if (blocks > 16384) blocks = 16384;
   patchify_kernel<T><<<blocks, 256, 0, s>>>(img, out, B, C, S, p);
   return hipGetLastError();
