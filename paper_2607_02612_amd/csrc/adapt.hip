@@ -74,59 +74,74 @@ __device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
 }
 
 // Cosine similarities of the A tokens (even patch slots) with the B tokens
-// (odd slots) of one sample, and the best B for every A.  The features are
-// the fp32 hidden states divided by their clamped norms; each is split into
-// bf16 hi + lo and the dot products take hi.hi' + hi.lo' + lo.hi' on
-// v_mfma_f32_16x16x32_bf16 with fp32 accumulation (absolute error of a
-// cosine <= ~1.2e-5, the dropped lo.lo' term included).  Wave w owns A rows
-// ag + 16w .. +15 against every B tile; lane l of an output tile holds
-// S[a = 4(l/16) + j][b = l%16].
+// (odd slots) of one sample, and the best B for every A.
+//
+// One pass over the features in chunks of SKC: every thread stages a fixed
+// set of (row, 4-feature) slots, splits the fp32 values into bf16 hi + lo,
+// and accumulates the row's sum of squares on the way; the dot products
+// take hi.hi' + hi.lo' + lo.hi' on v_mfma_f32_16x16x32_bf16 with fp32
+// accumulation (absolute error of a cosine <= ~1.2e-5, the dropped lo.lo'
+// term included).  The loads of chunk k+1 are issued before the MFMAs of
+// chunk k.  At the end the dots are divided by the clamped norms
+// max(||x||, 1e-12) of both tokens.  Wave w owns A rows ag + 16w .. +15
+// against every B tile; lane l of an output tile holds S[a = 4(l/16) + j]
+// [b = l%16].
+constexpr int SPT = ((SAG + AD_BMAX) * (SKC / 4) + AD_NT - 1) / AD_NT;  // slots / thread
+
 __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
-                                  int nA, int nB, const float* nrm,
-                                  float* bestsim, int* best, bf16_t* Ahi,
-                                  bf16_t* Alo, bf16_t* Bhi, bf16_t* Blo) {
+                                  int nA, int nB, float* nrm, float* bestsim,
+                                  int* best, bf16_t* Ahi, bf16_t* Alo,
+                                  bf16_t* Bhi, bf16_t* Blo) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c = lane & 15;
   const int nbt = (nB + 15) >> 4;
+  const int nslot = (SAG + nbt * 16) * (SKC / 4);
   for (int ag = 0; ag < nA; ag += SAG) {
+    // this thread's slots: row r = u / (SKC/4) (A rows first, then B rows)
+    const float* srow[SPT];
+    float ss[SPT];
+#pragma unroll
+    for (int w = 0; w < SPT; w++) {
+      const int u = tid + w * AD_NT;
+      const int r = u / (SKC / 4), q = (u % (SKC / 4)) * 4;
+      srow[w] = nullptr;
+      ss[w] = 0.f;
+      if (u < nslot) {
+        if (r < SAG) {
+          if (ag + r < nA) srow[w] = x + (size_t)(base + 1 + 2 * (ag + r)) * d + q;
+        } else if (r - SAG < nB) {
+          srow[w] = x + (size_t)(base + 2 + 2 * (r - SAG)) * d + q;
+        }
+      }
+    }
+    float4 cur[SPT];
+#pragma unroll
+    for (int w = 0; w < SPT; w++)
+      cur[w] = srow[w] ? *(const float4*)srow[w] : make_float4(0.f, 0.f, 0.f, 0.f);
     f32x4_t acc[SNBT];
 #pragma unroll
     for (int t = 0; t < SNBT; t++) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < d; k0 += SKC) {
       __syncthreads();
-      // stage normalised features as hi/lo bf16 (rows beyond the sets are 0)
-      for (int u = tid; u < (SAG + nbt * 16) * (SKC / 4); u += AD_NT) {
-        const int r = u / (SKC / 4), q = (u - r * (SKC / 4)) * 4;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        float inv = 0.f;
-        bf16_t* H;
-        bf16_t* Lo;
-        int rr;
-        if (r < SAG) {
-          const int aa = ag + r;
-          rr = r;
-          H = Ahi;
-          Lo = Alo;
-          if (aa < nA) {
-            v = *(const float4*)(x + (size_t)(base + 1 + 2 * aa) * d + k0 + q);
-            inv = nrm[2 * aa];
-          }
-        } else {
-          const int bb = r - SAG;
-          rr = bb;
-          H = Bhi;
-          Lo = Blo;
-          if (bb < nB) {
-            v = *(const float4*)(x + (size_t)(base + 2 + 2 * bb) * d + k0 + q);
-            inv = nrm[2 * bb + 1];
-          }
-        }
-        const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int w = 0; w < SPT; w++) {
+        const int u = tid + w * AD_NT;
+        if (u >= nslot) continue;
+        const int r = u / (SKC / 4), q = (u % (SKC / 4)) * 4;
+        bf16_t* H = r < SAG ? Ahi + r * SKP : Bhi + (r - SAG) * SKP;
+        bf16_t* Lo = r < SAG ? Alo + r * SKP : Blo + (r - SAG) * SKP;
+        const float e[4] = {cur[w].x, cur[w].y, cur[w].z, cur[w].w};
 #pragma unroll
         for (int z = 0; z < 4; z++) {
-          const float f = inv > 0.f ? e[z] / inv : 0.f;
-          split_bf16(f, H[rr * SKP + q + z], Lo[rr * SKP + q + z]);
+          ss[w] = fmaf(e[z], e[z], ss[w]);
+          split_bf16(e[z], H[q + z], Lo[q + z]);
         }
+      }
+      // prefetch the next chunk while this one is multiplied
+      if (k0 + SKC < d) {
+#pragma unroll
+        for (int w = 0; w < SPT; w++)
+          if (srow[w]) cur[w] = *(const float4*)(srow[w] + k0 + SKC);
       }
       __syncthreads();
       const bf16x8_t ah = *(const bf16x8_t*)(Ahi + (wave * 16 + c) * SKP + 8 * g);
@@ -142,17 +157,36 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
         }
       }
     }
-    // argmax over B for the lane's 4 A rows, ties to the lowest B index
+    // row norms: the SKC/4 threads of a row are adjacent lanes
+#pragma unroll
+    for (int w = 0; w < SPT; w++) {
+      float v = ss[w];
+#pragma unroll
+      for (int o = 1; o < SKC / 4; o <<= 1) v += __shfl_xor(v, o, 64);
+      const int u = tid + w * AD_NT;
+      const int r = u / (SKC / 4);
+      if (srow[w] && (u % (SKC / 4)) == 0) {
+        const int slot = r < SAG ? 2 * (ag + r) : 2 * (r - SAG) + 1;  // patch slot
+        nrm[slot] = fmaxf(sqrtf(v), 1e-12f);
+      }
+    }
+    __syncthreads();
+    // cosine = dot / (n_a n_b); argmax over B, ties to the lowest B index
 #pragma unroll
     for (int j = 0; j < 4; j++) {
+      const int aa = ag + wave * 16 + 4 * g + j;
+      const float na = aa < nA ? nrm[2 * aa] : 1.f;
       float bv = -INFINITY;
       int bi = 0x7fffffff;
 #pragma unroll
       for (int t = 0; t < SNBT; t++) {
         const int bb = t * 16 + c;
-        if (t < nbt && bb < nB && acc[t][j] > bv) {
-          bv = acc[t][j];
-          bi = bb;
+        if (t < nbt && bb < nB) {
+          const float v = acc[t][j] / (na * nrm[2 * bb + 1]);
+          if (v > bv) {
+            bv = v;
+            bi = bb;
+          }
         }
       }
 #pragma unroll
@@ -164,14 +198,13 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
           bi = oi;
         }
       }
-      const int aa = ag + wave * 16 + 4 * g + j;
       if (c == 0 && aa < nA) {
         bestsim[aa] = bv;
         best[aa] = bi < nB ? bi : 0;  // bi >= nB only with non-finite x
       }
     }
+    __syncthreads();
   }
-  __syncthreads();
 }
 
 __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
@@ -192,6 +225,12 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   __shared__ int clist[AD_AMAX];
   __shared__ float tmpf[AD_BMAX];
   __shared__ float tmps[AD_BMAX];
+  __shared__ int gid[AD_BMAX];
+  __shared__ int gdst[AD_BMAX];
+  __shared__ int gcnt[AD_BMAX];
+  __shared__ int goff[AD_BMAX + 1];
+  __shared__ int gsrc[AD_AMAX];
+  __shared__ int s_ng;
   __shared__ __attribute__((aligned(16))) bf16_t Ahi[SAG * SKP];
   __shared__ __attribute__((aligned(16))) bf16_t Alo[SAG * SKP];
   __shared__ __attribute__((aligned(16))) bf16_t Bhi[AD_BMAX * SKP];
@@ -224,15 +263,6 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   }
   const int nA = (N + 1) / 2, nB = N / 2;
   if (r > 0) {
-    // clamped L2 norms of the patch tokens
-    for (int j = wave; j < N; j += AD_NT / 64) {
-      const float* xr = a.x + (size_t)(base + 1 + j) * d;
-      float ss = 0.f;
-      for (int k = lane; k < d; k += 64) ss = fmaf(xr[k], xr[k], ss);
-      ss = wave_sum(ss);
-      if (lane == 0) nrm[j] = fmaxf(sqrtf(ss), 1e-12f);
-    }
-    __syncthreads();
     similarity_argmax(a.x, base, d, nA, nB, nrm, bestsim, best, Ahi, Alo, Bhi, Blo);
     // top-r of A by best similarity, ties to the lower A slot
     for (int aa = tid; aa < nA; aa += AD_NT) {
@@ -245,47 +275,68 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
       chosen[aa] = rank < r;
     }
     __syncthreads();
+    // group the chosen sources by destination: gdst[k] is the k-th B slot
+    // that receives sources, its sources (ascending A slot) are
+    // gsrc[goff[k] .. goff[k+1])
+    for (int bb = tid; bb < nB; bb += AD_NT) gid[bb] = -1;
+    __syncthreads();
     if (tid == 0) {
-      int n = 0;
+      int n = 0, ng = 0;
       for (int aa = 0; aa < nA; aa++)
-        if (chosen[aa]) clist[n++] = aa;
+        if (chosen[aa]) {
+          clist[n++] = aa;
+          const int bb = best[aa];
+          if (gid[bb] < 0) {
+            gid[bb] = ng;
+            gdst[ng] = bb;
+            gcnt[ng] = 0;
+            ng++;
+          }
+          gcnt[gid[bb]]++;
+        }
+      int run = 0;
+      for (int k = 0; k < ng; k++) {
+        goff[k] = run;
+        run += gcnt[k];
+        gcnt[k] = 0;
+      }
+      goff[ng] = run;
+      for (int q = 0; q < n; q++) {
+        const int k = gid[best[clist[q]]];
+        gsrc[goff[k] + gcnt[k]++] = clist[q];
+      }
+      s_ng = ng;
     }
     __syncthreads();
-    // size-weighted merge into each destination, sources in ascending order
-    for (int idx = tid; idx < nB * d; idx += AD_NT) {
-      const int bb = idx / d, f = idx - bb * d;
-      const size_t rowb = (size_t)(base + 2 + 2 * bb);
+    const int ng = s_ng;
+    // size-weighted merge into each receiving destination, sources ascending
+    for (int idx = tid; idx < ng * d; idx += AD_NT) {
+      const int k = idx / d, f = idx - k * d;
+      const size_t rowb = (size_t)(base + 2 + 2 * gdst[k]);
       float num = a.size[rowb] * a.x[rowb * d + f];
       float den = a.size[rowb];
-      bool has = false;
-      for (int q = 0; q < r; q++) {
-        const int aa = clist[q];
-        if (best[aa] == bb) {
-          const size_t rowa = (size_t)(base + 1 + 2 * aa);
-          num = num + a.size[rowa] * a.x[rowa * d + f];
-          den = den + a.size[rowa];
-          has = true;
-        }
+      for (int q = goff[k]; q < goff[k + 1]; q++) {
+        const size_t rowa = (size_t)(base + 1 + 2 * gsrc[q]);
+        num = num + a.size[rowa] * a.x[rowa * d + f];
+        den = den + a.size[rowa];
       }
-      if (has) a.x[rowb * d + f] = num / den;
+      a.x[rowb * d + f] = num / den;
     }
-    for (int bb = tid; bb < nB; bb += AD_NT) {
+    for (int k = tid; k < ng; k += AD_NT) {
+      const int bb = gdst[k];
       float den = a.size[base + 2 + 2 * bb];
       float s2 = a.isP ? sc[2 + 2 * bb] : 0.f;
-      for (int q = 0; q < r; q++) {
-        const int aa = clist[q];
-        if (best[aa] == bb) {
-          den = den + a.size[base + 1 + 2 * aa];
-          if (a.isP) s2 = s2 + sc[1 + 2 * aa];
-        }
+      for (int q = goff[k]; q < goff[k + 1]; q++) {
+        den = den + a.size[base + 1 + 2 * gsrc[q]];
+        if (a.isP) s2 = s2 + sc[1 + 2 * gsrc[q]];
       }
-      tmpf[bb] = den;
-      tmps[bb] = s2;
+      tmpf[k] = den;
+      tmps[k] = s2;
     }
     __syncthreads();
-    for (int bb = tid; bb < nB; bb += AD_NT) {
-      a.size[base + 2 + 2 * bb] = tmpf[bb];
-      if (a.isP) sc[2 + 2 * bb] = tmps[bb];
+    for (int k = tid; k < ng; k += AD_NT) {
+      a.size[base + 2 + 2 * gdst[k]] = tmpf[k];
+      if (a.isP) sc[2 + 2 * gdst[k]] = tmps[k];
     }
     for (int q = tid; q < r; q += AD_NT) {
       const int aa = clist[q];

@@ -146,6 +146,7 @@ int parse_blob(const void* blob, size_t bytes, Config& c,
     if (c.exit_mask >> (b - 1) & 1) c.exits.push_back(b);
   // limits of the kernels
   if (c.n0 + 1 > 640) return fail(FUSION_E_BLOB, "more than 640 tokens per sample");
+  if (c.patch % 4) return fail(FUSION_E_BLOB, "patch side must be a multiple of 4");
   if (c.d > 768 || c.d % 16) return fail(FUSION_E_BLOB, "width must be a multiple of 16 and <= 768");
   if (c.precision == 1 && (c.d % 64 || c.mlp % 64 || c.pdim % 64))
     return fail(FUSION_E_BLOB, "bf16 path needs width, MLP width and patch size multiples of 64");

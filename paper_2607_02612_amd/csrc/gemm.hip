@@ -136,6 +136,7 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
+template <int EPI>
 __global__ __launch_bounds__(256) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
     int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
@@ -223,18 +224,37 @@ __global__ __launch_bounds__(256) void gemm_mfma_bf16(
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
   }
+  // epilogue: the lane's column n is fixed per (i, j) block, rows vary
 #pragma unroll
-  for (int i = 0; i < 2; i++)
+  for (int j = 0; j < 2; j++) {
+    const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+    if (n >= N) continue;
+    const float bn = e.bias[n];
 #pragma unroll
-    for (int j = 0; j < 2; j++) {
-      const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-      if (n >= N) continue;
+    for (int i = 0; i < 2; i++) {
 #pragma unroll
       for (int q = 0; q < 16; q++) {
         const int r = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        if (r < M) epilogue<bf16_t>(e, r, n, acc[i][j][q]);
+        if (r >= M) continue;
+        const float v = acc[i][j][q] + bn;
+        if (EPI == EPI_STORE) {
+          ((bf16_t*)e.out)[(size_t)r * e.ldo + n] = f32_to_bf16(v);
+        } else if (EPI == EPI_GELU) {
+          ((bf16_t*)e.out)[(size_t)r * e.ldo + n] = f32_to_bf16(gelu_erf(v));
+        } else if (EPI == EPI_RESID) {
+          float* px = (float*)e.out + (size_t)r * e.ldo + n;
+          *px = *px + v;
+        } else if (EPI == EPI_F32) {
+          const int orow = e.rows ? e.rows[r] : r;
+          ((float*)e.out)[(size_t)orow * e.ldo + n] = v;
+        } else {  // EPI_PATCH
+          const int sidx = r / e.n0, jj = r - sidx * e.n0;
+          const size_t xr = (size_t)sidx * (e.n0 + 1) + 1 + jj;
+          ((float*)e.out)[xr * e.ldo + n] = v + e.pos[(size_t)(1 + jj) * e.ldo + n];
+        }
       }
     }
+  }
 }
 
 template <>
@@ -257,7 +277,14 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   if (K % KS != 0 || lda % 8 != 0 || K <= 0) return hipErrorInvalidValue;
   const int n_mt = (M_ub + MB - 1) / MB, n_nt = (N + NB - 1) / NB;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
-  gemm_mfma_bf16<<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e);
+  switch (e.mode) {
+    case EPI_STORE: gemm_mfma_bf16<EPI_STORE><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
+    case EPI_GELU: gemm_mfma_bf16<EPI_GELU><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
+    case EPI_RESID: gemm_mfma_bf16<EPI_RESID><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
+    case EPI_F32: gemm_mfma_bf16<EPI_F32><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
+    case EPI_PATCH: gemm_mfma_bf16<EPI_PATCH><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

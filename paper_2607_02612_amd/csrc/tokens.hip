@@ -52,34 +52,45 @@ hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
 }
 
 // images [B, C, S, S] -> patches [B*n0, C*p*p]; patch (gy, gx) in raster
-// order, vector element (c, ky, kx).  One work item copies the p contiguous
-// pixels of one (patch, channel, kernel row); index math in 32 bits (the
-// host checks that B * n0 * C * p fits).
+// order, vector element (c, ky, kx).  One thread moves 4 consecutive pixels
+// of a kernel row (p % 4 == 0): a 16-byte load and one vector store, with
+// consecutive threads on consecutive pixels; 32-bit index math (the host
+// checks that B * n0 * C * p * p / 4 fits).
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+  static __device__ __forceinline__ void put(float* d, float4 v) { *(float4*)d = v; }
+};
+template <> struct Vec4<bf16_t> {
+  static __device__ __forceinline__ void put(bf16_t* d, float4 v) {
+    uint2 u;
+    u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+    u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+    *(uint2*)d = u;
+  }
+};
+
 template <typename T>
 __global__ void patchify_kernel(const float* __restrict__ img, T* __restrict__ out,
                                 int B, int C, int S, int p) {
-  const int g = S / p, n0 = g * g;
-  const int items = B * n0 * C * p;
+  const int g = S / p, n0 = g * g, pd = C * p * p, q4 = pd / 4;
+  const int items = B * n0 * q4;
   for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < items;
        t += gridDim.x * blockDim.x) {
-    int rest = t;
-    const int ky = rest % p;
-    rest /= p;
-    const int c = rest % C;
-    const int row = rest / C;            // global patch row s * n0 + j
+    const int row = t / q4, e = (t - row * q4) * 4;
+    const int c = e / (p * p), rem = e - c * p * p;
+    const int ky = rem / p, kx = rem - ky * p;
     const int s = row / n0, j = row - s * n0;
     const int gy = j / g, gx = j - gy * g;
-    const float* src = img + (((size_t)s * C + c) * S + gy * p + ky) * S + gx * p;
-    T* dst = out + (size_t)row * (C * p * p) + (c * p + ky) * p;
-    for (int kx = 0; kx < p; kx++) dst[kx] = St<T>::put(src[kx]);
+    const float4 v = *(const float4*)(img + (((size_t)s * C + c) * S + gy * p + ky) * S + gx * p + kx);
+    Vec4<T>::put(out + (size_t)row * pd + e, v);
   }
 }
 
 template <typename T>
 hipError_t launch_patchify(const float* img, T* out, int B, int C, int S,
                            int p, hipStream_t s) {
-  const long items = (long)B * (S / p) * (S / p) * C * p;
-  if (items >= (1L << 31)) return hipErrorInvalidValue;
+  const long items = (long)B * (S / p) * (S / p) * C * p * p / 4;
+  if (items >= (1L << 31) || p % 4 != 0 || S % 4 != 0) return hipErrorInvalidValue;
   int blocks = (int)((items + 255) / 256);
   if (blocks > 16384) blocks = 16384;
   patchify_kernel<T><<<blocks, 256, 0, s>>>(img, out, B, C, S, p);
