@@ -299,14 +299,186 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
   }
 }
 
+// Resident variant for T <= 16 * MAXT <= 256 keys: one workgroup per (live
+// sample, head) stages K (padded rows) and V^T ([dim][key], built with an
+// 8x8 register transpose and 16-byte LDS stores) once; then each wave walks
+// the query tiles qt = wave, wave + 4, ... with no further barrier.  Per
+// query tile the arithmetic is the chunked kernel's: transposed scores with
+// the exact row maximum, then round(E) V with the key permutation.
+constexpr int RKS = 64 + 8;  // K row stride (bf16)
+
+template <int MAXT>
+__global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
+  constexpr int TP = MAXT * 16;      // padded keys
+  constexpr int TPE = ((MAXT + 1) / 2) * 32;  // keys covered by tile pairs
+  constexpr int VTS = TPE + 8;       // V^T row stride (bf16)
+  const int i = blockIdx.x, h = blockIdx.y;
+  if (i >= a.cnt->nlive) return;
+  const int base = a.cu[i], Tn = a.cu[i + 1] - base;
+  if (Tn > a.T_ub || Tn > TP) return;  // the host bound is exact
+  if (h == 0 && threadIdx.x == 0 && a.token_counts)
+    a.token_counts[a.live[i] * a.L + a.b0] = Tn;
+  const int d = a.d, ld = 3 * d;
+  const bf16_t* qkv = (const bf16_t*)a.qkv;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[TP * RKS];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[64 * VTS];
+  __shared__ float lnS[TP];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, c = lane & 15;
+  const int nkt = (Tn + 15) >> 4;
+
+  // ---- stage K rows (zero beyond T) and ln(size)
+  const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
+  for (int u = tid; u < nkt * 16 * 8; u += 256) {
+    const int r = u >> 3, cc = (u & 7) * 8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (r < Tn) v = *(const uint4*)(kg + (size_t)r * ld + cc);
+    *(uint4*)(Ks + r * RKS + cc) = v;
+  }
+  for (int j = tid; j < nkt * 16; j += 256)
+    lnS[j] = (j < Tn && a.prop_attn) ? logf(a.size[base + j]) : 0.f;
+  // ---- stage V^T: thread = 8 keys x 8 dims block, transposed in registers;
+  // staged up to an even number of key tiles (zeros past T), so the last
+  // tile pair of P V never reads outside the staged keys
+  const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
+  const int nkt2 = (nkt + 1) & ~1;
+  for (int u = tid; u < nkt2 * 2 * 8; u += 256) {
+    const int kb = u >> 3, db = (u & 7) * 8;   // keys 8kb.., dims db..
+    uint32_t in[8][4];
+#pragma unroll
+    for (int r = 0; r < 8; r++) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (kb * 8 + r < Tn) v = *(const uint4*)(vg + (size_t)(kb * 8 + r) * ld + db);
+      in[r][0] = v.x; in[r][1] = v.y; in[r][2] = v.z; in[r][3] = v.w;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+      uint32_t w[4];
+#pragma unroll
+      for (int q = 0; q < 4; q++) {
+        const uint32_t lo = (in[2 * q][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+        const uint32_t hi = (in[2 * q + 1][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+        w[q] = lo | (hi << 16);
+      }
+      *(uint4*)(Vt + (db + j) * VTS + kb * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+  __syncthreads();
+
+  bf16_t* out = (bf16_t*)a.out;
+  for (int qt = wave; qt < nkt; qt += 4) {
+    const int q0 = qt * 16;
+    bf16x8_t qop[2];
+    {
+      const int q = q0 + c;
+      const bf16_t* qr = qkv + (size_t)(base + q) * ld + h * 64;
+#pragma unroll
+      for (int hf = 0; hf < 2; hf++) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (q < Tn) v = *(const uint4*)(qr + hf * 32 + 8 * g);
+        qop[hf] = *(bf16x8_t*)&v;
+      }
+    }
+    f32x4_t S[MAXT];
+#pragma unroll
+    for (int t = 0; t < MAXT; t++) {
+      S[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      if (t < nkt) {
+        const bf16_t* kr = Ks + (t * 16 + c) * RKS + 8 * g;
+        const bf16x8_t k0 = *(const bf16x8_t*)kr;
+        const bf16x8_t k1 = *(const bf16x8_t*)(kr + 32);
+        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[0], S[t], 0, 0, 0);
+        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[1], S[t], 0, 0, 0);
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < MAXT; t++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int key = t * 16 + 4 * g + j;
+        float v = -INFINITY;
+        if (t < nkt && key < Tn) {
+          v = S[t][j] * a.scale;
+          if (a.prop_attn) v = v + lnS[key];
+        }
+        S[t][j] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float ls = 0.f;
+#pragma unroll
+    for (int t = 0; t < MAXT; t++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const float e = (t < nkt) ? expf(S[t][j] - mx) : 0.f;
+        S[t][j] = e;
+        ls += e;
+      }
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    if (a.cls_scores && q0 == 0 && c == 0) {
+      float* cs = a.cls_scores + ((size_t)i * a.H + h) * a.tmax;
+#pragma unroll
+      for (int t = 0; t < MAXT; t++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          const int key = t * 16 + 4 * g + j;
+          if (t < nkt && key < Tn) cs[key] = S[t][j] / ls;
+        }
+    }
+    f32x4_t O[4];
+#pragma unroll
+    for (int n = 0; n < 4; n++) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < (MAXT + 1) / 2; p++) {
+      const int t0 = 2 * p, t1 = 2 * p + 1;
+      if (t0 < nkt) {
+        union { bf16_t u[8]; bf16x8_t v; } cv;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          cv.u[j] = f32_to_bf16(S[t0][j]);
+          cv.u[4 + j] = (t1 < MAXT) ? f32_to_bf16(S[t1 < MAXT ? t1 : 0][j]) : (bf16_t)0;
+        }
+        const int kl = 32 * p + 4 * g;
+#pragma unroll
+        for (int n = 0; n < 4; n++) {
+          const bf16_t* vr = Vt + (n * 16 + c) * VTS + kl;
+          union { uint2 u[2]; bf16x8_t v; } vb;
+          vb.u[0] = *(const uint2*)vr;
+          vb.u[1] = *(const uint2*)(vr + 16);
+          O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cv.v, vb.v, O[n], 0, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int q = q0 + 4 * g + j;
+      const float l = __shfl(ls, 4 * g + j, 64);
+      if (q < Tn) {
+#pragma unroll
+        for (int n = 0; n < 4; n++)
+          out[(size_t)(base + q) * d + h * 64 + n * 16 + c] = f32_to_bf16(O[n][j] / l);
+      }
+    }
+  }
+}
+
 template <typename T>
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
   if (sizeof(T) == 2 && a.dh == 64) {
+    if (a.T_ub <= 16 * 13) {
+      attention_mfma_res<13><<<dim3(a.nlive_ub, a.H), 256, 0, s>>>(a);
+      return hipGetLastError();
+    }
+    if (a.T_ub <= 16 * 16) {
+      attention_mfma_res<16><<<dim3(a.nlive_ub, a.H), 256, 0, s>>>(a);
+      return hipGetLastError();
+    }
     dim3 grid(a.nlive_ub, a.H, (a.T_ub + 63) / 64);
-    if (a.T_ub <= 16 * 13)
-      attention_mfma<13><<<grid, 256, 0, s>>>(a);
-    else if (a.T_ub <= 16 * 40)
+    if (a.T_ub <= 16 * 40)
       attention_mfma<40><<<grid, 256, 0, s>>>(a);
     else
       return hipErrorInvalidValue;
