@@ -3,9 +3,12 @@
 // per-head CLS attention row that scores tokens for pruning.
 //
 // Softmax uses the exact row maximum: the full score row of a query is held
-// (LDS) before exponentiation.  E = exp(S - max), l = sum E in fp32, the
-// stored probabilities E are rounded to the storage type before they
-// multiply V, and O = (round(E) V) / l.
+// (LDS or registers) before exponentiation.  E = exp(S - max), l = sum E in
+// fp32, the stored probabilities E are rounded to the storage type before
+// they multiply V, and O = (round(E) V) / l.  The MFMA kernels evaluate the
+// exponent in base 2 with the hardware exp2: t = dot (scale log2 e) +
+// ln(size) log2 e, E = exp2(t - max t) (the same quantity up to the
+// rounding of the folded constants), and scale O by 1 / l.
 //
 // bf16 path with 64-wide heads: MFMA kernel below.  fp32 path (and any
 // other head width): one workgroup per (live sample, head); each of the 4
@@ -126,6 +129,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
+constexpr float kLog2e = 1.4426950408889634f;
 constexpr int AKC = 64;            // keys per LDS chunk
 constexpr int AKS = 64 + 8;        // K chunk row stride (bf16), dh = 64
 constexpr int AVS = AKC + 8;       // V^T chunk row stride (bf16)
@@ -140,6 +144,7 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
   if (h == 0 && qb == 0 && threadIdx.x == 0 && a.token_counts)
     a.token_counts[a.live[i] * a.L + a.b0] = Tn;
   const int d = a.d, ld = 3 * d;
+  const float sc2 = a.scale * kLog2e;
   const bf16_t* qkv = (const bf16_t*)a.qkv;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[AKC * AKS];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[64 * AVS];
@@ -152,7 +157,7 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
   const int nch = (Tn + AKC - 1) / AKC; // key chunks
 
   for (int j = tid; j < nkt * 16; j += 256)
-    lnS[j] = (j < Tn && a.prop_attn) ? logf(a.size[base + j]) : 0.f;
+    lnS[j] = (j < Tn && a.prop_attn) ? logf(a.size[base + j]) * kLog2e : 0.f;
 
   // Q^T operand: lane holds Q[q0 + c][8g .. 8g+7] and [32 + 8g ..]
   bf16x8_t qop[2];
@@ -202,10 +207,7 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
     for (int j = 0; j < 4; j++) {
       const int key = t * 16 + 4 * g + j;
       float v = -INFINITY;
-      if (t < nkt && key < Tn) {
-        v = S[t][j] * a.scale;
-        if (a.prop_attn) v = v + lnS[key];
-      }
+        if (t < nkt && key < Tn) v = fmaf(S[t][j], sc2, lnS[key]);
       S[t][j] = v;
       mx = fmaxf(mx, v);
     }
@@ -217,12 +219,13 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
   for (int t = 0; t < MAXT; t++)
 #pragma unroll
     for (int j = 0; j < 4; j++) {
-      const float e = (t < nkt) ? expf(S[t][j] - mx) : 0.f;
+      const float e = (t < nkt) ? __builtin_amdgcn_exp2f(S[t][j] - mx) : 0.f;
       S[t][j] = e;
       ls += e;
     }
   ls += __shfl_xor(ls, 16, 64);
   ls += __shfl_xor(ls, 32, 64);
+  const float rl = 1.0f / ls;
 
   if (a.cls_scores && q0 == 0 && c == 0) {
     float* cs = a.cls_scores + ((size_t)i * a.H + h) * a.tmax;
@@ -231,7 +234,7 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; j++) {
         const int key = t * 16 + 4 * g + j;
-        if (t < nkt && key < Tn) cs[key] = S[t][j] / ls;
+        if (t < nkt && key < Tn) cs[key] = S[t][j] * rl;
       }
   }
 
@@ -290,11 +293,11 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
 #pragma unroll
   for (int j = 0; j < 4; j++) {
     const int q = q0 + 4 * g + j;
-    const float l = __shfl(ls, 4 * g + j, 64);
+    const float l = __shfl(rl, 4 * g + j, 64);
     if (q < Tn) {
 #pragma unroll
       for (int n = 0; n < 4; n++)
-        out[(size_t)(base + q) * d + h * 64 + n * 16 + c] = f32_to_bf16(O[n][j] / l);
+        out[(size_t)(base + q) * d + h * 64 + n * 16 + c] = f32_to_bf16(O[n][j] * l);
     }
   }
 }
@@ -319,6 +322,7 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
   if (h == 0 && threadIdx.x == 0 && a.token_counts)
     a.token_counts[a.live[i] * a.L + a.b0] = Tn;
   const int d = a.d, ld = 3 * d;
+  const float sc2 = a.scale * kLog2e;
   const bf16_t* qkv = (const bf16_t*)a.qkv;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[TP * RKS];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[64 * VTS];
@@ -336,7 +340,7 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
     *(uint4*)(Ks + r * RKS + cc) = v;
   }
   for (int j = tid; j < nkt * 16; j += 256)
-    lnS[j] = (j < Tn && a.prop_attn) ? logf(a.size[base + j]) : 0.f;
+    lnS[j] = (j < Tn && a.prop_attn) ? logf(a.size[base + j]) * kLog2e : 0.f;
   // ---- stage V^T: thread = 8 keys x 8 dims block, transposed in registers;
   // staged up to an even number of key tiles (zeros past T), so the last
   // tile pair of P V never reads outside the staged keys
@@ -398,10 +402,7 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
       for (int j = 0; j < 4; j++) {
         const int key = t * 16 + 4 * g + j;
         float v = -INFINITY;
-        if (t < nkt && key < Tn) {
-          v = S[t][j] * a.scale;
-          if (a.prop_attn) v = v + lnS[key];
-        }
+        if (t < nkt && key < Tn) v = fmaf(S[t][j], sc2, lnS[key]);
         S[t][j] = v;
         mx = fmaxf(mx, v);
       }
@@ -412,12 +413,13 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
     for (int t = 0; t < MAXT; t++)
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        const float e = (t < nkt) ? expf(S[t][j] - mx) : 0.f;
+        const float e = (t < nkt) ? __builtin_amdgcn_exp2f(S[t][j] - mx) : 0.f;
         S[t][j] = e;
         ls += e;
       }
     ls += __shfl_xor(ls, 16, 64);
     ls += __shfl_xor(ls, 32, 64);
+    const float rl = 1.0f / ls;
     if (a.cls_scores && q0 == 0 && c == 0) {
       float* cs = a.cls_scores + ((size_t)i * a.H + h) * a.tmax;
 #pragma unroll
@@ -425,7 +427,7 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; j++) {
           const int key = t * 16 + 4 * g + j;
-          if (t < nkt && key < Tn) cs[key] = S[t][j] / ls;
+          if (t < nkt && key < Tn) cs[key] = S[t][j] * rl;
         }
     }
     f32x4_t O[4];
@@ -455,11 +457,11 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; j++) {
       const int q = q0 + 4 * g + j;
-      const float l = __shfl(ls, 4 * g + j, 64);
+      const float l = __shfl(rl, 4 * g + j, 64);
       if (q < Tn) {
 #pragma unroll
         for (int n = 0; n < 4; n++)
-          out[(size_t)(base + q) * d + h * 64 + n * 16 + c] = f32_to_bf16(O[n][j] / l);
+          out[(size_t)(base + q) * d + h * 64 + n * 16 + c] = f32_to_bf16(O[n][j] * l);
       }
     }
   }
