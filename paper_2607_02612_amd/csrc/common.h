@@ -14,11 +14,11 @@ struct LiveCounts {
   int M;      // packed token rows of the live samples
 };
 
-// float -> bfloat16, round to nearest, ties to even.
+// float -> bfloat16, round to nearest, ties to even: gfx950's
+// v_cvt_pk_bf16_f32 (bit-identical to the integer formulation
+// u + 0x7FFF + ((u >> 16) & 1) >> 16 on finite inputs, subnormals included).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+  return __builtin_bit_cast(bf16_t, (__bf16)f);
 }
 __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
   return __uint_as_float(((uint32_t)h) << 16);
@@ -78,9 +78,26 @@ __device__ __forceinline__ int block_sum256_i(int v, int* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// Exact GELU, 0.5 v (1 + erf(v / sqrt 2)).
+// erf by the rational approximation 7.1.26 of Abramowitz & Stegun
+// (Handbook of Mathematical Functions): for x >= 0,
+//   erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2),
+//   t = 1 / (1 + p x),
+// absolute error <= 1.5e-7 (plus fp32 rounding); odd in x.
+__device__ __forceinline__ float erf_as7126(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
+  float y = fmaf(t, 1.061405429f, -1.453152027f);
+  y = fmaf(t, y, 1.421413741f);
+  y = fmaf(t, y, -0.284496736f);
+  y = fmaf(t, y, 0.254829592f);
+  const float e = __builtin_amdgcn_exp2f(-(ax * ax) * 1.4426950408889634f);
+  const float r = fmaf(-(t * y), e, 1.0f);
+  return copysignf(r, x);
+}
+
+// GELU with the exact (erf) form, 0.5 v (1 + erf(v / sqrt 2)).
 __device__ __forceinline__ float gelu_erf(float v) {
-  return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
+  return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f));
 }
 
 }  // namespace fusion

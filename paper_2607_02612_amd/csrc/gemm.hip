@@ -224,7 +224,52 @@ __global__ __launch_bounds__(256) void gemm_mfma_bf16(
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
   }
-  // epilogue: the lane's column n is fixed per (i, j) block, rows vary
+  // epilogue: the lane's column n is fixed per (i, j) block, rows vary.
+  // For the bf16 outputs and the fp32 residual, lanes l and l^1 (adjacent
+  // columns) exchange one value per row pair (q, q+1) so that each writes
+  // two adjacent columns of one row: the even lane row q, the odd lane row
+  // q+1.
+  if (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_RESID) {
+    const bool odd = lane & 1;
+#pragma unroll
+    for (int j = 0; j < 2; j++) {
+      const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+      const int nc = odd ? n - 1 : n;  // first column written by this lane
+      const float b0 = nc < N ? e.bias[nc] : 0.f;
+      const float b1 = nc + 1 < N ? e.bias[nc + 1] : 0.f;
+#pragma unroll
+      for (int i = 0; i < 2; i++) {
+#pragma unroll
+        for (int q = 0; q < 16; q += 2) {
+          const int rq = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+          const float give = odd ? acc[i][j][q] : acc[i][j][q + 1];
+          const float got = __shfl_xor(give, 1, 64);
+          // even lane: row rq, (own, partner); odd lane: row rq+1, (partner, own)
+          float v0 = odd ? got : acc[i][j][q];
+          float v1 = odd ? acc[i][j][q + 1] : got;
+          const int r = odd ? rq + 1 : rq;
+          if (r >= M || nc >= N) continue;
+          v0 += b0;
+          v1 += b1;
+          if (EPI == EPI_RESID) {
+            float2* px = (float2*)((float*)e.out + (size_t)r * e.ldo + nc);
+            float2 xv = *px;
+            xv.x = xv.x + v0;
+            xv.y = xv.y + v1;
+            *px = xv;
+          } else {
+            if (EPI == EPI_GELU) {
+              v0 = gelu_erf(v0);
+              v1 = gelu_erf(v1);
+            }
+            const uint32_t pk = (uint32_t)f32_to_bf16(v0) | ((uint32_t)f32_to_bf16(v1) << 16);
+            *(uint32_t*)((bf16_t*)e.out + (size_t)r * e.ldo + nc) = pk;
+          }
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < 2; j++) {
     const int n = n0 + wn * 64 + j * 32 + (lane & 31);
@@ -237,14 +282,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_bf16(
         const int r = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
         if (r >= M) continue;
         const float v = acc[i][j][q] + bn;
-        if (EPI == EPI_STORE) {
-          ((bf16_t*)e.out)[(size_t)r * e.ldo + n] = f32_to_bf16(v);
-        } else if (EPI == EPI_GELU) {
-          ((bf16_t*)e.out)[(size_t)r * e.ldo + n] = f32_to_bf16(gelu_erf(v));
-        } else if (EPI == EPI_RESID) {
-          float* px = (float*)e.out + (size_t)r * e.ldo + n;
-          *px = *px + v;
-        } else if (EPI == EPI_F32) {
+        if (EPI == EPI_F32) {
           const int orow = e.rows ? e.rows[r] : r;
           ((float*)e.out)[(size_t)orow * e.ldo + n] = v;
         } else {  // EPI_PATCH
@@ -272,9 +310,13 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
                                int N, int K, const int* M_dev, int M_host,
                                int M_ub, const Epi& e, hipStream_t s) {
   if (M_ub <= 0) return hipSuccess;
-  // The K steps need K % 32 == 0 and 16-byte aligned rows; the model
-  // creation rejects bf16 shapes that do not satisfy this.
+  // The K steps need K % 32 == 0 and 16-byte aligned rows; the paired
+  // epilogue stores need an even N and output stride.  The model creation
+  // rejects bf16 shapes that do not satisfy this.
   if (K % KS != 0 || lda % 8 != 0 || K <= 0) return hipErrorInvalidValue;
+  if ((e.mode == EPI_STORE || e.mode == EPI_GELU || e.mode == EPI_RESID) &&
+      (N % 2 != 0 || e.ldo % 2 != 0))
+    return hipErrorInvalidValue;
   const int n_mt = (M_ub + MB - 1) / MB, n_nt = (N + NB - 1) / NB;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
   switch (e.mode) {
