@@ -217,83 +217,62 @@ __global__ __launch_bounds__(256) void gemm_mfma_bf16(
         const int r = wn * 64 + j * 32 + (lane & 31);
         b[j] = *(const bf16x8_t*)(Bb + r * ROWB + ((c ^ ((r >> 2) & 3)) << 4));
       }
+      // transposed product: acc[i][j] holds C^T, so lane l owns output row
+      // m = .. + (l % 32) and columns n = .. + 8 (q / 4) + 4 (l / 32) + q % 4
 #pragma unroll
       for (int i = 0; i < 2; i++)
 #pragma unroll
         for (int j = 0; j < 2; j++)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
     }
   }
-  // epilogue: the lane's column n is fixed per (i, j) block, rows vary.
-  // For the bf16 outputs and the fp32 residual, lanes l and l^1 (adjacent
-  // columns) exchange one value per row pair (q, q+1) so that each writes
-  // two adjacent columns of one row: the even lane row q, the odd lane row
-  // q+1.
-  if (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_RESID) {
-    const bool odd = lane & 1;
+  // epilogue: four consecutive columns per register quad -> vector stores
+#pragma unroll
+  for (int i = 0; i < 2; i++) {
+    const int m = m0 + wm * 64 + i * 32 + (lane & 31);
+    if (m >= M) continue;
+    size_t orow = (size_t)m;
+    int pj = 0;
+    if (EPI == EPI_F32) orow = e.rows ? (size_t)e.rows[m] : (size_t)m;
+    if (EPI == EPI_PATCH) {
+      const int sidx = m / e.n0;
+      pj = m - sidx * e.n0;
+      orow = (size_t)sidx * (e.n0 + 1) + 1 + pj;
+    }
 #pragma unroll
     for (int j = 0; j < 2; j++) {
-      const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-      const int nc = odd ? n - 1 : n;  // first column written by this lane
-      const float b0 = nc < N ? e.bias[nc] : 0.f;
-      const float b1 = nc + 1 < N ? e.bias[nc + 1] : 0.f;
 #pragma unroll
-      for (int i = 0; i < 2; i++) {
-#pragma unroll
-        for (int q = 0; q < 16; q += 2) {
-          const int rq = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-          const float give = odd ? acc[i][j][q] : acc[i][j][q + 1];
-          const float got = __shfl_xor(give, 1, 64);
-          // even lane: row rq, (own, partner); odd lane: row rq+1, (partner, own)
-          float v0 = odd ? got : acc[i][j][q];
-          float v1 = odd ? acc[i][j][q + 1] : got;
-          const int r = odd ? rq + 1 : rq;
-          if (r >= M || nc >= N) continue;
-          v0 += b0;
-          v1 += b1;
-          if (EPI == EPI_RESID) {
-            float2* px = (float2*)((float*)e.out + (size_t)r * e.ldo + nc);
-            float2 xv = *px;
-            xv.x = xv.x + v0;
-            xv.y = xv.y + v1;
-            *px = xv;
-          } else {
-            if (EPI == EPI_GELU) {
-              v0 = gelu_erf(v0);
-              v1 = gelu_erf(v1);
-            }
-            const uint32_t pk = (uint32_t)f32_to_bf16(v0) | ((uint32_t)f32_to_bf16(v1) << 16);
-            *(uint32_t*)((bf16_t*)e.out + (size_t)r * e.ldo + nc) = pk;
+      for (int q4 = 0; q4 < 4; q4++) {
+        const int nb = n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
+        if (nb >= N) continue;
+        const float4 bv = *(const float4*)(e.bias + nb);
+        float v0 = acc[i][j][4 * q4 + 0] + bv.x, v1 = acc[i][j][4 * q4 + 1] + bv.y;
+        float v2 = acc[i][j][4 * q4 + 2] + bv.z, v3 = acc[i][j][4 * q4 + 3] + bv.w;
+        if (EPI == EPI_STORE || EPI == EPI_GELU) {
+          if (EPI == EPI_GELU) {
+            v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
           }
-        }
-      }
-    }
-    return;
-  }
-#pragma unroll
-  for (int j = 0; j < 2; j++) {
-    const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-    if (n >= N) continue;
-    const float bn = e.bias[n];
-#pragma unroll
-    for (int i = 0; i < 2; i++) {
-#pragma unroll
-      for (int q = 0; q < 16; q++) {
-        const int r = m0 + wm * 64 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        if (r >= M) continue;
-        const float v = acc[i][j][q] + bn;
-        if (EPI == EPI_F32) {
-          const int orow = e.rows ? e.rows[r] : r;
-          ((float*)e.out)[(size_t)orow * e.ldo + n] = v;
-        } else {  // EPI_PATCH
-          const int sidx = r / e.n0, jj = r - sidx * e.n0;
-          const size_t xr = (size_t)sidx * (e.n0 + 1) + 1 + jj;
-          ((float*)e.out)[xr * e.ldo + n] = v + e.pos[(size_t)(1 + jj) * e.ldo + n];
+          uint2 pk;
+          pk.x = (uint32_t)f32_to_bf16(v0) | ((uint32_t)f32_to_bf16(v1) << 16);
+          pk.y = (uint32_t)f32_to_bf16(v2) | ((uint32_t)f32_to_bf16(v3) << 16);
+          *(uint2*)((bf16_t*)e.out + orow * e.ldo + nb) = pk;
+        } else if (EPI == EPI_RESID) {
+          float4* px = (float4*)((float*)e.out + orow * e.ldo + nb);
+          float4 xv = *px;
+          xv.x = xv.x + v0; xv.y = xv.y + v1; xv.z = xv.z + v2; xv.w = xv.w + v3;
+          *px = xv;
+        } else if (EPI == EPI_F32) {
+          *(float4*)((float*)e.out + orow * e.ldo + nb) = make_float4(v0, v1, v2, v3);
+        } else {  // EPI_PATCH: + position embedding of token 1 + pj
+          const float4 pv = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + nb);
+          *(float4*)((float*)e.out + orow * e.ldo + nb) =
+              make_float4(v0 + pv.x, v1 + pv.y, v2 + pv.z, v3 + pv.w);
         }
       }
     }
   }
 }
+
 
 template <>
 hipError_t launch_gemm<float>(const float* A, int lda, const float* W, int N,
@@ -310,13 +289,11 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
                                int N, int K, const int* M_dev, int M_host,
                                int M_ub, const Epi& e, hipStream_t s) {
   if (M_ub <= 0) return hipSuccess;
-  // The K steps need K % 32 == 0 and 16-byte aligned rows; the paired
-  // epilogue stores need an even N and output stride.  The model creation
-  // rejects bf16 shapes that do not satisfy this.
+  // The K steps need K % 32 == 0 and 16-byte aligned rows; the vector
+  // epilogue needs N and the output stride to be multiples of 4.  The model
+  // creation rejects bf16 shapes that do not satisfy this.
   if (K % KS != 0 || lda % 8 != 0 || K <= 0) return hipErrorInvalidValue;
-  if ((e.mode == EPI_STORE || e.mode == EPI_GELU || e.mode == EPI_RESID) &&
-      (N % 2 != 0 || e.ldo % 2 != 0))
-    return hipErrorInvalidValue;
+  if (N % 4 != 0 || e.ldo % 4 != 0) return hipErrorInvalidValue;
   const int n_mt = (M_ub + MB - 1) / MB, n_nt = (N + NB - 1) / NB;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
   switch (e.mode) {
