@@ -95,6 +95,8 @@ def main():
     ap.add_argument("--workload", default="deit_s")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=48)
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the 0 %% early-exit setting (for profiler runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -144,6 +146,8 @@ def main():
 
     sweep = {}
     for e_rate in sorted(th):
+        if args.headline_only and e_rate != 0.0:
+            continue
         sweep[e_rate] = timed(th[e_rate])
     head = sweep[0.0]
 

@@ -370,19 +370,23 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
   __syncthreads();
 
   bf16_t* out = (bf16_t*)a.out;
+  // Q^T operand of the wave's first query tile; the next tile's is fetched
+  // while the current one is processed
+  uint4 qnext[2];
+  auto load_q = [&](int qt, uint4* dstq) {
+    const int q = qt * 16 + c;
+    const bf16_t* qr = qkv + (size_t)(base + q) * ld + h * 64;
+#pragma unroll
+    for (int hf = 0; hf < 2; hf++)
+      dstq[hf] = (q < Tn) ? *(const uint4*)(qr + hf * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
+  };
+  load_q(wave, qnext);
   for (int qt = wave; qt < nkt; qt += 4) {
     const int q0 = qt * 16;
     bf16x8_t qop[2];
-    {
-      const int q = q0 + c;
-      const bf16_t* qr = qkv + (size_t)(base + q) * ld + h * 64;
-#pragma unroll
-      for (int hf = 0; hf < 2; hf++) {
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (q < Tn) v = *(const uint4*)(qr + hf * 32 + 8 * g);
-        qop[hf] = *(bf16x8_t*)&v;
-      }
-    }
+    qop[0] = *(bf16x8_t*)&qnext[0];
+    qop[1] = *(bf16x8_t*)&qnext[1];
+    if (qt + 4 < nkt) load_q(qt + 4, qnext);
     f32x4_t S[MAXT];
 #pragma unroll
     for (int t = 0; t < MAXT; t++) {

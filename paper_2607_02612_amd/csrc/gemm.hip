@@ -98,8 +98,9 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 }
 
 // ------------------------------------------------------------ bf16 MFMA --
-// 128x128 output tile per workgroup, 4 waves in a 2x2 grid, each wave a
-// 64x64 sub-tile of 2x2 v_mfma_f32_32x32x16_bf16 blocks.
+// MBx128 output tile per workgroup (MB = 128: 4 waves in a 2x2 grid; MB =
+// 64: 2 waves side by side), each wave a 64x64 sub-tile of 2x2
+// v_mfma_f32_32x32x16_bf16 blocks.
 //
 // K is consumed in steps of 32.  A and W tiles reach LDS through the gfx950
 // asynchronous global->LDS path (global_load_lds_dwordx4): each wave-wide
@@ -121,11 +122,9 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // Operand layout of v_mfma_f32_32x32x16_bf16 (64 lanes): lane l supplies
 // A[row l%32][k 8*(l/32) .. +7] and B[k 8*(l/32) .. +7][col l%32]; result
 // element q of lane l is C[8*(q/4) + 4*(l/32) + q%4][l%32].
-constexpr int MB = 128, NB = 128, KS = 32, NSTG = 3;
+constexpr int NB = 128, KS = 32, NSTG = 3;
 constexpr int ROWB = KS * 2;                 // bytes per staged row
-constexpr int STGB = (MB + NB) * ROWB;       // bytes per stage
 constexpr int NXCD = 8;
-constexpr int DMA_PER_WAVE = (MB + NB) / 16 / 4;
 
 __device__ __forceinline__ void dma16(const void* gptr, unsigned lds_byte_addr) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
@@ -136,14 +135,20 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
-template <int EPI>
-__global__ __launch_bounds__(256) void gemm_mfma_bf16(
+// MB = 128 (4 waves, 2x2) or 64 (2 waves, 1x2) rows per tile; the smaller
+// tile is chosen when 128-row tiles would leave CUs idle.
+template <int EPI, int MB>
+__global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
     int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
+  constexpr int NWV = MB / 64 * 2;                    // waves
+  constexpr int STGB = (MB + NB) * ROWB;              // bytes per stage
+  constexpr int DMA_PER_WAVE = (MB + NB) / 16 / NWV;  // 16-row blocks per wave
   const int M = M_dev ? *M_dev : M_host;
   const int n_nt = (N + NB - 1) / NB;
   const int id = blockIdx.x;
   const int xcd = id % NXCD, local = id / NXCD;
+  static_assert((MB + NB) / 16 % NWV == 0, "stage split");
   const int mt = (local / n_nt) * NXCD + xcd, nt = local % n_nt;
   const int m0 = mt * MB, n0 = nt * NB;
   if (mt >= n_mt || m0 >= M) return;
@@ -294,16 +299,25 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   // creation rejects bf16 shapes that do not satisfy this.
   if (K % KS != 0 || lda % 8 != 0 || K <= 0) return hipErrorInvalidValue;
   if (N % 4 != 0 || e.ldo % 4 != 0) return hipErrorInvalidValue;
-  const int n_mt = (M_ub + MB - 1) / MB, n_nt = (N + NB - 1) / NB;
+  const int n_nt = (N + NB - 1) / NB;
+  const bool small = (long)((M_ub + 127) / 128) * n_nt < 512;
+  const int mb = small ? 64 : 128;
+  const int n_mt = (M_ub + mb - 1) / mb;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
+#define FUSION_GEMM_LAUNCH(E)                                                          \
+  if (small)                                                                          \
+    gemm_mfma_bf16<E, 64><<<grid, 128, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
+  else                                                                                \
+    gemm_mfma_bf16<E, 128><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e)
   switch (e.mode) {
-    case EPI_STORE: gemm_mfma_bf16<EPI_STORE><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
-    case EPI_GELU: gemm_mfma_bf16<EPI_GELU><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
-    case EPI_RESID: gemm_mfma_bf16<EPI_RESID><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
-    case EPI_F32: gemm_mfma_bf16<EPI_F32><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
-    case EPI_PATCH: gemm_mfma_bf16<EPI_PATCH><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); break;
+    case EPI_STORE: FUSION_GEMM_LAUNCH(EPI_STORE); break;
+    case EPI_GELU: FUSION_GEMM_LAUNCH(EPI_GELU); break;
+    case EPI_RESID: FUSION_GEMM_LAUNCH(EPI_RESID); break;
+    case EPI_F32: FUSION_GEMM_LAUNCH(EPI_F32); break;
+    case EPI_PATCH: FUSION_GEMM_LAUNCH(EPI_PATCH); break;
     default: return hipErrorInvalidValue;
   }
+#undef FUSION_GEMM_LAUNCH
   return hipGetLastError();
 }
 
