@@ -66,6 +66,26 @@ def kernel_work(cfg, counts):
     return w
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (profiles/traffic.json), or None if it was taken on other kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    entry = t.get("kernels", {}).get(kernel)
+    if not entry:
+        return None
+    src = os.path.join(ROOT, "paper_2607_02612_amd", "csrc", entry["source"])
+    with open(src, "rb") as f:
+        digest = hashlib.sha256(f.read()).hexdigest()
+    if digest != entry["source_sha256"]:
+        return None
+    return entry["bytes_per_launch"]
+
+
 def cpu_baseline(cfg, W, imgs, n):
     """The oracle on the first n images (bounded sample), images/s."""
     from oracle import fusion_oracle as fo
@@ -97,6 +117,9 @@ def main():
     ap.add_argument("--cpu-images", type=int, default=48)
     ap.add_argument("--headline-only", action="store_true",
                     help="time only the 0 %% early-exit setting (for profiler runs)")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run one 256 MiB device-to-device copy, whose HBM "
+                         "counters calibrate FETCH_SIZE / WRITE_SIZE")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -144,6 +167,14 @@ def main():
                     early_exit=float((eb < cfg["L"]).mean()),
                     mean_tokens=float(counts[counts > 0].mean()), counts=counts)
 
+    if args.calib_copy:
+        src = torch.empty(64 << 20, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     sweep = {}
     for e_rate in sorted(th):
         if args.headline_only and e_rate != 0.0:
@@ -180,7 +211,7 @@ def main():
     dk = kernels[dom]
     roofline = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                 "peak": BF16_PEAK / 1e12, "unit": "TFLOP/s",
-                "frac": dk["frac_bf16_peak"], "traffic": None}
+                "frac": dk["frac_bf16_peak"], "traffic": measured_traffic(dom)}
 
     line = {
         "metric": "images/sec at DeiT-S b=256 bf16 (1 GPU); % bf16 MFMA peak on executed FLOPs",
