@@ -67,6 +67,26 @@ __device__ __forceinline__ int bsum_i(int v, int* red) {
   return s;
 }
 
+// Stream compaction over the workgroup (one candidate per thread): writes
+// the indices `v` of the threads with `f` set to out[0 ..) in thread order
+// and returns their count.  red >= AD_NT / 64 ints.
+__device__ __forceinline__ int block_compact(bool f, int v, int* out, int* red) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const unsigned long long msk = __ballot(f);
+  __syncthreads();
+  if (lane == 0) red[wave] = __popcll(msk);
+  __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < AD_NT / 64; w++) {
+    off += w < wave ? red[w] : 0;
+    tot += red[w];
+  }
+  if (f) out[off + __popcll(msk & ((1ull << lane) - 1ull))] = v;
+  __syncthreads();
+  return tot;
+}
+
 // Split a float into bf16 hi + lo with hi + lo = v to about 2^-17 relative.
 __device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
   hi = f32_to_bf16(v);
@@ -217,20 +237,17 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   const size_t tr_row = (size_t)(a.b - 1) * a.B + orig;
 
   __shared__ float sc[AD_TMAX];
+  __shared__ float szs[AD_TMAX];
   __shared__ int keepf[AD_TMAX];
   __shared__ float nrm[AD_TMAX];
   __shared__ float bestsim[AD_AMAX];
   __shared__ int best[AD_AMAX];
   __shared__ int chosen[AD_AMAX];
   __shared__ int clist[AD_AMAX];
-  __shared__ float tmpf[AD_BMAX];
-  __shared__ float tmps[AD_BMAX];
-  __shared__ int gid[AD_BMAX];
-  __shared__ int gdst[AD_BMAX];
-  __shared__ int gcnt[AD_BMAX];
-  __shared__ int goff[AD_BMAX + 1];
-  __shared__ int gsrc[AD_AMAX];
-  __shared__ int s_ng;
+  __shared__ int cdst[AD_AMAX];
+  __shared__ int glead[AD_AMAX];
+  __shared__ float tmpf[AD_AMAX];
+  __shared__ float tmps[AD_AMAX];
   __shared__ __attribute__((aligned(16))) bf16_t Ahi[SAG * SKP];
   __shared__ __attribute__((aligned(16))) bf16_t Alo[SAG * SKP];
   __shared__ __attribute__((aligned(16))) bf16_t Bhi[AD_BMAX * SKP];
@@ -238,7 +255,10 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   __shared__ float red[16];
   __shared__ int ired[16];
 
-  for (int t = tid; t < T; t += AD_NT) keepf[t] = 1;
+  for (int t = tid; t < T; t += AD_NT) {
+    keepf[t] = 1;
+    szs[t] = a.size[base + t];
+  }
   if (a.isP) {
     for (int t = tid; t < T; t += AD_NT) {
       float s = a.cls_scores[((size_t)i * a.H) * a.tmax + t];
@@ -275,68 +295,61 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
       chosen[aa] = rank < r;
     }
     __syncthreads();
-    // group the chosen sources by destination: gdst[k] is the k-th B slot
-    // that receives sources, its sources (ascending A slot) are
-    // gsrc[goff[k] .. goff[k+1])
-    for (int bb = tid; bb < nB; bb += AD_NT) gid[bb] = -1;
+    // chosen sources in ascending A slot: clist[0 .. r)
+    block_compact(tid < nA && chosen[tid], tid, clist, ired);
+    // destination of each; a source leads its group when no earlier chosen
+    // source has the same destination.  Groups are merged independently,
+    // each summing its sources in ascending A slot.
+    for (int q = tid; q < r; q += AD_NT) cdst[q] = best[clist[q]];
     __syncthreads();
-    if (tid == 0) {
-      int n = 0, ng = 0;
-      for (int aa = 0; aa < nA; aa++)
-        if (chosen[aa]) {
-          clist[n++] = aa;
-          const int bb = best[aa];
-          if (gid[bb] < 0) {
-            gid[bb] = ng;
-            gdst[ng] = bb;
-            gcnt[ng] = 0;
-            ng++;
-          }
-          gcnt[gid[bb]]++;
-        }
-      int run = 0;
-      for (int k = 0; k < ng; k++) {
-        goff[k] = run;
-        run += gcnt[k];
-        gcnt[k] = 0;
-      }
-      goff[ng] = run;
-      for (int q = 0; q < n; q++) {
-        const int k = gid[best[clist[q]]];
-        gsrc[goff[k] + gcnt[k]++] = clist[q];
-      }
-      s_ng = ng;
+    bool lead = false;
+    if (tid < r) {
+      const int bb = cdst[tid];
+      lead = true;
+      for (int q2 = 0; q2 < tid; q2++) lead = lead && (cdst[q2] != bb);
     }
-    __syncthreads();
-    const int ng = s_ng;
-    // size-weighted merge into each receiving destination, sources ascending
-    for (int idx = tid; idx < ng * d; idx += AD_NT) {
-      const int k = idx / d, f = idx - k * d;
-      const size_t rowb = (size_t)(base + 2 + 2 * gdst[k]);
-      float num = a.size[rowb] * a.x[rowb * d + f];
-      float den = a.size[rowb];
-      for (int q = goff[k]; q < goff[k + 1]; q++) {
-        const size_t rowa = (size_t)(base + 1 + 2 * gsrc[q]);
-        num = num + a.size[rowa] * a.x[rowa * d + f];
-        den = den + a.size[rowa];
+    const int ng = block_compact(lead, tid, glead, ired);
+    // size-weighted merge into each receiving destination (16-byte pieces)
+    const int d4 = d / 4;
+    float4* x4 = (float4*)a.x;
+    for (int idx = tid; idx < ng * d4; idx += AD_NT) {
+      const int k = idx / d4, f = idx - k * d4;
+      const int q0 = glead[k], bb = cdst[q0];
+      const size_t rowb = (size_t)(base + 2 + 2 * bb);
+      const float sb = szs[2 + 2 * bb];
+      const float4 xb = x4[rowb * d4 + f];
+      float4 num = make_float4(sb * xb.x, sb * xb.y, sb * xb.z, sb * xb.w);
+      float den = sb;
+      for (int q = q0; q < r; q++) {
+        if (cdst[q] != bb) continue;
+        const int aa = clist[q];
+        const float sa = szs[1 + 2 * aa];
+        const float4 xa = x4[(size_t)(base + 1 + 2 * aa) * d4 + f];
+        num.x = num.x + sa * xa.x;
+        num.y = num.y + sa * xa.y;
+        num.z = num.z + sa * xa.z;
+        num.w = num.w + sa * xa.w;
+        den = den + sa;
       }
-      a.x[rowb * d + f] = num / den;
+      x4[rowb * d4 + f] = make_float4(num.x / den, num.y / den, num.z / den, num.w / den);
     }
     for (int k = tid; k < ng; k += AD_NT) {
-      const int bb = gdst[k];
-      float den = a.size[base + 2 + 2 * bb];
+      const int q0 = glead[k], bb = cdst[q0];
+      float den = szs[2 + 2 * bb];
       float s2 = a.isP ? sc[2 + 2 * bb] : 0.f;
-      for (int q = goff[k]; q < goff[k + 1]; q++) {
-        den = den + a.size[base + 1 + 2 * gsrc[q]];
-        if (a.isP) s2 = s2 + sc[1 + 2 * gsrc[q]];
+      for (int q = q0; q < r; q++) {
+        if (cdst[q] != bb) continue;
+        den = den + szs[1 + 2 * clist[q]];
+        if (a.isP) s2 = s2 + sc[1 + 2 * clist[q]];
       }
       tmpf[k] = den;
       tmps[k] = s2;
     }
     __syncthreads();
     for (int k = tid; k < ng; k += AD_NT) {
-      a.size[base + 2 + 2 * gdst[k]] = tmpf[k];
-      if (a.isP) sc[2 + 2 * gdst[k]] = tmps[k];
+      const int bb = cdst[glead[k]];
+      a.size[base + 2 + 2 * bb] = tmpf[k];
+      if (a.isP) sc[2 + 2 * bb] = tmps[k];
     }
     for (int q = tid; q < r; q += AD_NT) {
       const int aa = clist[q];

@@ -331,30 +331,42 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
   const int g = lane >> 4, c = lane & 15;
   const int nkt = (Tn + 15) >> 4;
 
-  // ---- stage K rows (zero beyond T) and ln(size)
+  // ---- staging: every global load (K rows, V rows, token sizes) is issued
+  // before the first LDS write, so the workgroup waits for one memory
+  // latency instead of one per loop trip
+  static_assert(MAXT <= 16, "one V block and one size per thread");
+  constexpr int KU = (TP * 8 + 255) / 256;  // 16-byte K pieces per thread
   const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
-  for (int u = tid; u < nkt * 16 * 8; u += 256) {
-    const int r = u >> 3, cc = (u & 7) * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < Tn) v = *(const uint4*)(kg + (size_t)r * ld + cc);
-    *(uint4*)(Ks + r * RKS + cc) = v;
-  }
-  for (int j = tid; j < nkt * 16; j += 256)
-    lnS[j] = (j < Tn && a.prop_attn) ? logf(a.size[base + j]) * kLog2e : 0.f;
-  // ---- stage V^T: thread = 8 keys x 8 dims block, transposed in registers;
-  // staged up to an even number of key tiles (zeros past T), so the last
-  // tile pair of P V never reads outside the staged keys
   const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
   const int nkt2 = (nkt + 1) & ~1;
-  for (int u = tid; u < nkt2 * 2 * 8; u += 256) {
-    const int kb = u >> 3, db = (u & 7) * 8;   // keys 8kb.., dims db..
-    uint32_t in[8][4];
+  uint4 kin[KU];
 #pragma unroll
-    for (int r = 0; r < 8; r++) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (kb * 8 + r < Tn) v = *(const uint4*)(vg + (size_t)(kb * 8 + r) * ld + db);
-      in[r][0] = v.x; in[r][1] = v.y; in[r][2] = v.z; in[r][3] = v.w;
-    }
+  for (int w = 0; w < KU; w++) {
+    const int u = tid + w * 256;
+    const int r = u >> 3, cc = (u & 7) * 8;
+    kin[w] = make_uint4(0, 0, 0, 0);
+    if (u < nkt * 16 * 8 && r < Tn) kin[w] = *(const uint4*)(kg + (size_t)r * ld + cc);
+  }
+  // V^T: thread = 8 keys x 8 dims block, transposed in registers; staged up
+  // to an even number of key tiles (zeros past T), so the last tile pair of
+  // P V never reads outside the staged keys
+  const int kb = tid >> 3, db = (tid & 7) * 8;   // keys 8kb.., dims db..
+  const bool vth = tid < nkt2 * 2 * 8;
+  uint32_t in[8][4];
+#pragma unroll
+  for (int r = 0; r < 8; r++) {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (vth && kb * 8 + r < Tn) v = *(const uint4*)(vg + (size_t)(kb * 8 + r) * ld + db);
+    in[r][0] = v.x; in[r][1] = v.y; in[r][2] = v.z; in[r][3] = v.w;
+  }
+  const bool sth = tid < nkt * 16;
+  const float sz = (sth && tid < Tn && a.prop_attn) ? a.size[base + tid] : 1.f;
+#pragma unroll
+  for (int w = 0; w < KU; w++) {
+    const int u = tid + w * 256;
+    if (u < nkt * 16 * 8) *(uint4*)(Ks + (u >> 3) * RKS + (u & 7) * 8) = kin[w];
+  }
+  if (vth) {
 #pragma unroll
     for (int j = 0; j < 8; j++) {
       uint32_t w[4];
@@ -367,6 +379,7 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
       *(uint4*)(Vt + (db + j) * VTS + kb * 8) = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }
+  if (sth) lnS[tid] = (tid < Tn && a.prop_attn) ? logf(sz) * kLog2e : 0.f;
   __syncthreads();
 
   bf16_t* out = (bf16_t*)a.out;

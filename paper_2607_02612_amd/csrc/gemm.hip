@@ -102,18 +102,26 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // 64: 2 waves side by side), each wave a 64x64 sub-tile of 2x2
 // v_mfma_f32_32x32x16_bf16 blocks.
 //
-// K is consumed in steps of 32.  A and W tiles reach LDS through the gfx950
-// asynchronous global->LDS path (global_load_lds_dwordx4): each wave-wide
-// instruction writes 64 lanes x 16 bytes contiguously, i.e. 16 rows of 64
-// bytes, without passing through VGPRs, so NSTG = 3 K steps are in flight
-// in a ring of LDS stages while the matrix cores work on the oldest one.
-// The loads are issued from inline assembly and their completion is awaited
-// with explicit vmcnt counts (a compiler-visible LDS DMA would make every
-// LDS read wait for all outstanding loads).  Rows are stored with their four
-// 16-byte chunks XOR-permuted by (row / 4) % 4, which makes the per-lane
-// 16-byte operand reads of 16 consecutive rows hit 16 disjoint bank groups.
-// Rows past M or N are clamped to the last valid row for the loads (every
-// address stays in bounds) and masked in the epilogue.
+// K is consumed in steps of KSV = 32 (three LDS stages) or 64 (two stages,
+// for long K).  A and W tiles reach LDS through the gfx950 asynchronous
+// global->LDS path (global_load_lds_dwordx4): each wave-wide instruction
+// writes 64 lanes x 16 bytes contiguously, i.e. 16 rows of 64 bytes or 8
+// rows of 128 bytes, without passing through VGPRs, so later K steps are in
+// flight while the matrix cores work on the current one (two or three
+// workgroups share a CU and cover each other's load latency).  The loads
+// are issued from inline assembly and their completion is awaited with
+// explicit vmcnt counts (a compiler-visible LDS DMA would make every LDS
+// read wait for all outstanding loads).  The 16-byte chunks of a staged row
+// are XOR-permuted (by (row / 4) % 4 for 64-byte rows, (row / 2) % 8 for
+// 128-byte rows), which makes the per-lane 16-byte operand reads of 16
+// consecutive rows hit 16 disjoint bank groups.  Rows past M or N are
+// clamped to the last valid row for the loads (every address stays in
+// bounds) and masked in the epilogue.
+//
+// Epilogue: bf16 outputs are staged through LDS (the drained K ring) so
+// that global stores are whole 256-byte row segments instead of 16-byte
+// pieces of 32 different rows; the fp32 residual update reads and writes x
+// directly (16 bytes per lane).
 //
 // Tile order: blocks are dispatched round-robin over the 8 XCDs (block id %
 // 8); the linear id is remapped so that each XCD walks whole row panels (all
@@ -122,9 +130,13 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // Operand layout of v_mfma_f32_32x32x16_bf16 (64 lanes): lane l supplies
 // A[row l%32][k 8*(l/32) .. +7] and B[k 8*(l/32) .. +7][col l%32]; result
 // element q of lane l is C[8*(q/4) + 4*(l/32) + q%4][l%32].
-constexpr int NB = 128, KS = 32, NSTG = 3;
-constexpr int ROWB = KS * 2;                 // bytes per staged row
+constexpr int NB = 128;
 constexpr int NXCD = 8;
+
+template <int KSV>
+__device__ __forceinline__ int kslot(int r, int c) {
+  return KSV == 32 ? (c ^ ((r >> 2) & 3)) : (c ^ ((r >> 1) & 7));
+}
 
 __device__ __forceinline__ void dma16(const void* gptr, unsigned lds_byte_addr) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
@@ -136,19 +148,25 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // MB = 128 (4 waves, 2x2) or 64 (2 waves, 1x2) rows per tile; the smaller
-// tile is chosen when 128-row tiles would leave CUs idle.
-template <int EPI, int MB>
+// tile is chosen when 128-row tiles would leave CUs idle.  KSV = K step.
+template <int EPI, int MB, int KSV>
 __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
     int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
+  constexpr int KS = KSV, NSTG = KSV == 64 ? 2 : 3;
+  constexpr int ROWB = KS * 2;                        // bytes per staged row
+  constexpr int CPR = KS / 8;                         // 16-byte chunks per staged row
+  constexpr int RPI = 64 / CPR;                       // rows per DMA instruction
   constexpr int NWV = MB / 64 * 2;                    // waves
+  constexpr int NT = NWV * 64;                        // threads
   constexpr int STGB = (MB + NB) * ROWB;              // bytes per stage
-  constexpr int DMA_PER_WAVE = (MB + NB) / 16 / NWV;  // 16-row blocks per wave
+  constexpr int DMA_PER_WAVE = (MB + NB) / RPI / NWV; // DMA instructions per wave and stage
+  static_assert((MB + NB) / RPI % NWV == 0, "stage split");
+  static_assert(MB * NB * 2 <= NSTG * STGB, "epilogue staging fits");
   const int M = M_dev ? *M_dev : M_host;
   const int n_nt = (N + NB - 1) / NB;
   const int id = blockIdx.x;
   const int xcd = id % NXCD, local = id / NXCD;
-  static_assert((MB + NB) / 16 % NWV == 0, "stage split");
   const int mt = (local / n_nt) * NXCD + xcd, nt = local % n_nt;
   const int m0 = mt * MB, n0 = nt * NB;
   if (mt >= n_mt || m0 >= M) return;
@@ -165,23 +183,23 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
       for (int q = 0; q < 16; q++) acc[i][j][q] = 0.f;
 
   // this lane's source row and LDS slot for each of the wave's DMA
-  // instructions (16-row blocks: A rows first, then W rows)
+  // instructions (8-row blocks: A rows first, then W rows)
   const bf16_t* src[DMA_PER_WAVE];
   unsigned dst[DMA_PER_WAVE];
 #pragma unroll
   for (int u = 0; u < DMA_PER_WAVE; u++) {
     const int q = wave * DMA_PER_WAVE + u;
-    const bool isA = q < MB / 16;
-    const int r = (isA ? q : q - MB / 16) * 16 + (lane >> 2);
-    const int chunk = (lane & 3) ^ ((r >> 2) & 3);
+    const bool isA = q < MB / RPI;
+    const int r = (isA ? q : q - MB / RPI) * RPI + lane / CPR;
+    const int chunk = kslot<KSV>(r, lane % CPR);
     if (isA) {
       const int gr = min(m0 + r, M - 1);
       src[u] = A + (size_t)gr * lda + chunk * 8;
-      dst[u] = q * 16 * ROWB;
+      dst[u] = q * RPI * ROWB;
     } else {
       const int gr = min(n0 + r, N - 1);
       src[u] = W + (size_t)gr * K + chunk * 8;
-      dst[u] = MB * ROWB + (q - MB / 16) * 16 * ROWB;
+      dst[u] = MB * ROWB + (q - MB / RPI) * RPI * ROWB;
     }
   }
   const int nk = K / KS;
@@ -194,7 +212,7 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
     }
   for (int kt = 0; kt < nk; kt++) {
     // stage kt has landed once at most the later stages are outstanding
-    if (kt + 1 < nk)
+    if (NSTG > 2 && kt + NSTG - 2 < nk)
       wait_vm<DMA_PER_WAVE * (NSTG - 2)>();
     else
       wait_vm<0>();
@@ -215,12 +233,12 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
 #pragma unroll
       for (int i = 0; i < 2; i++) {
         const int r = wm * 64 + i * 32 + (lane & 31);
-        a[i] = *(const bf16x8_t*)(Ab + r * ROWB + ((c ^ ((r >> 2) & 3)) << 4));
+        a[i] = *(const bf16x8_t*)(Ab + r * ROWB + (kslot<KSV>(r, c) << 4));
       }
 #pragma unroll
       for (int j = 0; j < 2; j++) {
         const int r = wn * 64 + j * 32 + (lane & 31);
-        b[j] = *(const bf16x8_t*)(Bb + r * ROWB + ((c ^ ((r >> 2) & 3)) << 4));
+        b[j] = *(const bf16x8_t*)(Bb + r * ROWB + (kslot<KSV>(r, c) << 4));
       }
       // transposed product: acc[i][j] holds C^T, so lane l owns output row
       // m = .. + (l % 32) and columns n = .. + 8 (q / 4) + 4 (l / 32) + q % 4
@@ -231,7 +249,46 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
     }
   }
-  // epilogue: four consecutive columns per register quad -> vector stores
+
+  if (EPI == EPI_STORE || EPI == EPI_GELU) {
+    // bf16 tile -> LDS (256-byte rows, 16-byte chunk c stored at c ^ (row % 16))
+    // -> global, 16 lanes per 256-byte row segment
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; i++) {
+      const int r = wm * 64 + i * 32 + (lane & 31);
+#pragma unroll
+      for (int j = 0; j < 2; j++) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; q4++) {
+          const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
+          if (n0 + c >= N) continue;
+          const float4 bv = *(const float4*)(e.bias + n0 + c);
+          float v0 = acc[i][j][4 * q4 + 0] + bv.x, v1 = acc[i][j][4 * q4 + 1] + bv.y;
+          float v2 = acc[i][j][4 * q4 + 2] + bv.z, v3 = acc[i][j][4 * q4 + 3] + bv.w;
+          if (EPI == EPI_GELU) {
+            v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
+          }
+          uint2 pk;
+          pk.x = (uint32_t)f32_to_bf16(v0) | ((uint32_t)f32_to_bf16(v1) << 16);
+          pk.y = (uint32_t)f32_to_bf16(v2) | ((uint32_t)f32_to_bf16(v3) << 16);
+          *(uint2*)(smem + r * (NB * 2) + (((c >> 3) ^ (r & 15)) << 4) + ((c >> 2) & 1) * 8) = pk;
+        }
+      }
+    }
+    __syncthreads();
+    bf16_t* out = (bf16_t*)e.out;
+    for (int t = tid; t < MB * (NB / 8); t += NT) {
+      const int r = t >> 4, cc = t & 15;
+      const int m = m0 + r, n = n0 + cc * 8;
+      if (m < M && n < N)
+        *(uint4*)(out + (size_t)m * e.ldo + n) =
+            *(const uint4*)(smem + r * (NB * 2) + ((cc ^ (r & 15)) << 4));
+    }
+    return;
+  }
+  // residual update, fp32 logits (row scatter) and the patch embedding:
+  // direct vector accesses
 #pragma unroll
   for (int i = 0; i < 2; i++) {
     const int m = m0 + wm * 64 + i * 32 + (lane & 31);
@@ -251,17 +308,9 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
         const int nb = n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
         if (nb >= N) continue;
         const float4 bv = *(const float4*)(e.bias + nb);
-        float v0 = acc[i][j][4 * q4 + 0] + bv.x, v1 = acc[i][j][4 * q4 + 1] + bv.y;
-        float v2 = acc[i][j][4 * q4 + 2] + bv.z, v3 = acc[i][j][4 * q4 + 3] + bv.w;
-        if (EPI == EPI_STORE || EPI == EPI_GELU) {
-          if (EPI == EPI_GELU) {
-            v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
-          }
-          uint2 pk;
-          pk.x = (uint32_t)f32_to_bf16(v0) | ((uint32_t)f32_to_bf16(v1) << 16);
-          pk.y = (uint32_t)f32_to_bf16(v2) | ((uint32_t)f32_to_bf16(v3) << 16);
-          *(uint2*)((bf16_t*)e.out + orow * e.ldo + nb) = pk;
-        } else if (EPI == EPI_RESID) {
+        const float v0 = acc[i][j][4 * q4 + 0] + bv.x, v1 = acc[i][j][4 * q4 + 1] + bv.y;
+        const float v2 = acc[i][j][4 * q4 + 2] + bv.z, v3 = acc[i][j][4 * q4 + 3] + bv.w;
+        if (EPI == EPI_RESID) {
           float4* px = (float4*)((float*)e.out + orow * e.ldo + nb);
           float4 xv = *px;
           xv.x = xv.x + v0; xv.y = xv.y + v1; xv.z = xv.z + v2; xv.w = xv.w + v3;
@@ -295,20 +344,28 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
                                int M_ub, const Epi& e, hipStream_t s) {
   if (M_ub <= 0) return hipSuccess;
   // The K steps need K % 32 == 0 and 16-byte aligned rows; the vector
-  // epilogue needs N and the output stride to be multiples of 4.  The model
-  // creation rejects bf16 shapes that do not satisfy this.
-  if (K % KS != 0 || lda % 8 != 0 || K <= 0) return hipErrorInvalidValue;
+  // epilogues need N and the output stride to be multiples of 8 (bf16
+  // outputs) or 4 (fp32 outputs).  The model creation rejects bf16 shapes
+  // that do not satisfy this.
+  if (K % 32 != 0 || lda % 8 != 0 || K <= 0) return hipErrorInvalidValue;
   if (N % 4 != 0 || e.ldo % 4 != 0) return hipErrorInvalidValue;
+  if ((e.mode == EPI_STORE || e.mode == EPI_GELU) && (N % 8 != 0 || e.ldo % 8 != 0))
+    return hipErrorInvalidValue;
   const int n_nt = (N + NB - 1) / NB;
   const bool small = (long)((M_ub + 127) / 128) * n_nt < 512;
   const int mb = small ? 64 : 128;
   const int n_mt = (M_ub + mb - 1) / mb;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
-#define FUSION_GEMM_LAUNCH(E)                                                          \
-  if (small)                                                                          \
-    gemm_mfma_bf16<E, 64><<<grid, 128, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
-  else                                                                                \
-    gemm_mfma_bf16<E, 128><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e)
+  // long K on 128-row tiles: 64-wide K steps (half the barriers); otherwise
+  // 32-wide steps with three stages (three workgroups per CU)
+  const bool k64 = !small && K % 64 == 0 && K >= 1024;
+#define FUSION_GEMM_LAUNCH(E)                                                                 \
+  if (small)                                                                                 \
+    gemm_mfma_bf16<E, 64, 32><<<grid, 128, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
+  else if (k64)                                                                              \
+    gemm_mfma_bf16<E, 128, 64><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
+  else                                                                                       \
+    gemm_mfma_bf16<E, 128, 32><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e)
   switch (e.mode) {
     case EPI_STORE: FUSION_GEMM_LAUNCH(EPI_STORE); break;
     case EPI_GELU: FUSION_GEMM_LAUNCH(EPI_GELU); break;
