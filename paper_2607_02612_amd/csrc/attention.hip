@@ -303,18 +303,31 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
 }
 
 // Resident variant for T <= 16 * MAXT <= 256 keys: one workgroup per (live
-// sample, head) stages K (padded rows) and V^T ([dim][key], built with an
-// 8x8 register transpose and 16-byte LDS stores) once; then each wave walks
-// the query tiles qt = wave, wave + 4, ... with no further barrier.  Per
+// sample, head) stages K and V^T ([dim][key], built with an 8x8 register
+// transpose and 16-byte LDS stores) once; then each of its 8 waves walks the
+// query tiles qt = wave, wave + 8, ... with no further barrier.  Per
 // query tile the arithmetic is the chunked kernel's: transposed scores with
 // the exact row maximum, then round(E) V with the key permutation.
-constexpr int RKS = 64 + 8;  // K row stride (bf16)
+//
+// K rows are stored unpadded (128 bytes) with their eight 16-byte chunks
+// XOR-permuted by row % 8, so the per-lane 16-byte reads of 16 rows are
+// free of bank conflicts.
+//
+// The key loops run over all MAXT tiles with no per-tile condition: K and
+// V^T are zero past the sample's T keys and the additive key term is -inf
+// there (so those probabilities are exactly 0).  The host picks MAXT =
+// ceil(T_ub / 16), so at most the tiles between T and the bound are idle.
+// The output product is taken transposed (V^T . E^T), so a lane holds four
+// consecutive head dimensions of one query and stores them as 8 bytes.
+constexpr int RES_NT = 512;  // 8 waves share the staged K and V^T
 
 template <int MAXT>
-__global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
-  constexpr int TP = MAXT * 16;      // padded keys
-  constexpr int TPE = ((MAXT + 1) / 2) * 32;  // keys covered by tile pairs
-  constexpr int VTS = TPE + 8;       // V^T row stride (bf16)
+__global__ __launch_bounds__(RES_NT, 4) void attention_mfma_res(AttnArgs a) {
+  static_assert(MAXT >= 1 && MAXT <= 16, "resident key range");
+  constexpr int TP = MAXT * 16;               // padded keys
+  constexpr int NP = (MAXT + 1) / 2;          // key tile pairs
+  constexpr int TPE = NP * 32;                // keys covered by tile pairs
+  constexpr int VTS = TPE + 8;                // V^T row stride (bf16)
   const int i = blockIdx.x, h = blockIdx.y;
   if (i >= a.cnt->nlive) return;
   const int base = a.cu[i], Tn = a.cu[i + 1] - base;
@@ -324,9 +337,10 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
   const int d = a.d, ld = 3 * d;
   const float sc2 = a.scale * kLog2e;
   const bf16_t* qkv = (const bf16_t*)a.qkv;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[TP * RKS];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[TP * 64];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[64 * VTS];
-  __shared__ float lnS[TP];
+  __shared__ __attribute__((aligned(16))) float lnS[TP];
+  __shared__ __attribute__((aligned(16))) float clsP[TP];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c = lane & 15;
   const int nkt = (Tn + 15) >> 4;
@@ -334,55 +348,53 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
   // ---- staging: every global load (K rows, V rows, token sizes) is issued
   // before the first LDS write, so the workgroup waits for one memory
   // latency instead of one per loop trip
-  static_assert(MAXT <= 16, "one V block and one size per thread");
-  constexpr int KU = (TP * 8 + 255) / 256;  // 16-byte K pieces per thread
+  constexpr int KU = (TP * 8 + RES_NT - 1) / RES_NT;  // 16-byte K pieces per thread
   const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
   const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
-  const int nkt2 = (nkt + 1) & ~1;
   uint4 kin[KU];
 #pragma unroll
   for (int w = 0; w < KU; w++) {
-    const int u = tid + w * 256;
+    const int u = tid + w * RES_NT;
     const int r = u >> 3, cc = (u & 7) * 8;
     kin[w] = make_uint4(0, 0, 0, 0);
-    if (u < nkt * 16 * 8 && r < Tn) kin[w] = *(const uint4*)(kg + (size_t)r * ld + cc);
+    if (u < TP * 8 && r < Tn) kin[w] = *(const uint4*)(kg + (size_t)r * ld + cc);
   }
-  // V^T: thread = 8 keys x 8 dims block, transposed in registers; staged up
-  // to an even number of key tiles (zeros past T), so the last tile pair of
-  // P V never reads outside the staged keys
-  const int kb = tid >> 3, db = (tid & 7) * 8;   // keys 8kb.., dims db..
-  const bool vth = tid < nkt2 * 2 * 8;
-  uint32_t in[8][4];
+  // V^T: thread = 4 keys x 8 dims block, transposed in registers
+  const int kb = tid >> 3, db = (tid & 7) * 8;   // keys 4kb.., dims db..
+  const bool vth = tid < 2 * TPE;
+  uint32_t in[4][4];
 #pragma unroll
-  for (int r = 0; r < 8; r++) {
+  for (int r = 0; r < 4; r++) {
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (vth && kb * 8 + r < Tn) v = *(const uint4*)(vg + (size_t)(kb * 8 + r) * ld + db);
+    if (vth && kb * 4 + r < Tn) v = *(const uint4*)(vg + (size_t)(kb * 4 + r) * ld + db);
     in[r][0] = v.x; in[r][1] = v.y; in[r][2] = v.z; in[r][3] = v.w;
   }
-  const bool sth = tid < nkt * 16;
-  const float sz = (sth && tid < Tn && a.prop_attn) ? a.size[base + tid] : 1.f;
+  const float sz = (tid < Tn && a.prop_attn) ? a.size[base + tid] : 1.f;
 #pragma unroll
   for (int w = 0; w < KU; w++) {
-    const int u = tid + w * 256;
-    if (u < nkt * 16 * 8) *(uint4*)(Ks + (u >> 3) * RKS + (u & 7) * 8) = kin[w];
+    const int u = tid + w * RES_NT;
+    if (u < TP * 8) *(uint4*)(Ks + (u >> 3) * 64 + (((u & 7) ^ ((u >> 3) & 7)) << 3)) = kin[w];
   }
   if (vth) {
 #pragma unroll
     for (int j = 0; j < 8; j++) {
-      uint32_t w[4];
+      uint32_t w[2];
 #pragma unroll
-      for (int q = 0; q < 4; q++) {
+      for (int q = 0; q < 2; q++) {
         const uint32_t lo = (in[2 * q][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
         const uint32_t hi = (in[2 * q + 1][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
         w[q] = lo | (hi << 16);
       }
-      *(uint4*)(Vt + (db + j) * VTS + kb * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+      *(uint2*)(Vt + (db + j) * VTS + kb * 4) = make_uint2(w[0], w[1]);
     }
   }
-  if (sth) lnS[tid] = (tid < Tn && a.prop_attn) ? logf(sz) * kLog2e : 0.f;
+  // key term of the base-2 scores: log2(size) (0 without proportional
+  // attention), -inf past the sample's keys
+  if (tid < TP) lnS[tid] = tid < Tn ? logf(sz) * kLog2e : -INFINITY;
   __syncthreads();
 
   bf16_t* out = (bf16_t*)a.out;
+  const bool want_cls = a.cls_scores != nullptr;
   // Q^T operand of the wave's first query tile; the next tile's is fetched
   // while the current one is processed
   uint4 qnext[2];
@@ -394,93 +406,111 @@ __global__ __launch_bounds__(256) void attention_mfma_res(AttnArgs a) {
       dstq[hf] = (q < Tn) ? *(const uint4*)(qr + hf * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
   };
   load_q(wave, qnext);
-  for (int qt = wave; qt < nkt; qt += 4) {
+  for (int qt = wave; qt < nkt; qt += RES_NT / 64) {
     const int q0 = qt * 16;
     bf16x8_t qop[2];
     qop[0] = *(bf16x8_t*)&qnext[0];
     qop[1] = *(bf16x8_t*)&qnext[1];
-    if (qt + 4 < nkt) load_q(qt + 4, qnext);
+    if (qt + RES_NT / 64 < nkt) load_q(qt + RES_NT / 64, qnext);
+    // S^T tiles: lane (g, c) holds keys 16t + 4g + j of query q0 + c.  The
+    // K operands are read two tiles ahead; the scheduling barriers keep the
+    // compiler from hoisting every read (which would exhaust the registers).
     f32x4_t S[MAXT];
+    bf16x8_t kf[3][2];
+    auto load_k = [&](int t, bf16x8_t* dstk) {
+      const int r = t * 16 + c;
+      const bf16_t* kr = Ks + r * 64;
+      dstk[0] = *(const bf16x8_t*)(kr + ((g ^ (r & 7)) << 3));
+      dstk[1] = *(const bf16x8_t*)(kr + (((4 + g) ^ (r & 7)) << 3));
+    };
+    load_k(0, kf[0]);
+    if (MAXT > 1) load_k(1, kf[1]);
 #pragma unroll
     for (int t = 0; t < MAXT; t++) {
-      S[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      if (t < nkt) {
-        const bf16_t* kr = Ks + (t * 16 + c) * RKS + 8 * g;
-        const bf16x8_t k0 = *(const bf16x8_t*)kr;
-        const bf16x8_t k1 = *(const bf16x8_t*)(kr + 32);
-        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[0], S[t], 0, 0, 0);
-        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[1], S[t], 0, 0, 0);
-      }
+      if (t + 2 < MAXT) load_k(t + 2, kf[(t + 2) % 3]);
+      S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[t % 3][0], qop[0],
+                                                      f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+      S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[t % 3][1], qop[1], S[t], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     float mx = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < MAXT; t++)
-#pragma unroll
-      for (int j = 0; j < 4; j++) {
-        const int key = t * 16 + 4 * g + j;
-        float v = -INFINITY;
-        if (t < nkt && key < Tn) v = fmaf(S[t][j], sc2, lnS[key]);
-        S[t][j] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    for (int t = 0; t < MAXT; t++) {
+      const float4 ks = *(const float4*)(lnS + t * 16 + 4 * g);
+      S[t][0] = fmaf(S[t][0], sc2, ks.x);
+      S[t][1] = fmaf(S[t][1], sc2, ks.y);
+      S[t][2] = fmaf(S[t][2], sc2, ks.z);
+      S[t][3] = fmaf(S[t][3], sc2, ks.w);
+      mx = fmaxf(mx, fmaxf(fmaxf(S[t][0], S[t][1]), fmaxf(S[t][2], S[t][3])));
+    }
+    mx = max_xor32(max_xor16(mx));
     float ls = 0.f;
 #pragma unroll
     for (int t = 0; t < MAXT; t++)
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        const float e = (t < nkt) ? __builtin_amdgcn_exp2f(S[t][j] - mx) : 0.f;
+        const float e = __builtin_amdgcn_exp2f(S[t][j] - mx);
         S[t][j] = e;
         ls += e;
       }
-    ls += __shfl_xor(ls, 16, 64);
-    ls += __shfl_xor(ls, 32, 64);
+    ls = sum_xor32(sum_xor16(ls));
     const float rl = 1.0f / ls;
-    if (a.cls_scores && q0 == 0 && c == 0) {
-      float* cs = a.cls_scores + ((size_t)i * a.H + h) * a.tmax;
+    if (want_cls && q0 == 0 && c == 0) {
 #pragma unroll
       for (int t = 0; t < MAXT; t++)
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-          const int key = t * 16 + 4 * g + j;
-          if (t < nkt && key < Tn) cs[key] = S[t][j] * rl;
-        }
+        *(float4*)(clsP + t * 16 + 4 * g) =
+            make_float4(S[t][0] * rl, S[t][1] * rl, S[t][2] * rl, S[t][3] * rl);
     }
+    // O^T = V^T . E^T: lane (g, c) accumulates dims 16n + 4g + j of query q0 + c
     f32x4_t O[4];
 #pragma unroll
     for (int n = 0; n < 4; n++) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    union VB { uint2 u[2]; bf16x8_t v; };
+    VB vb[2][4];
+    auto load_v = [&](int p, VB* dstv) {
 #pragma unroll
-    for (int p = 0; p < (MAXT + 1) / 2; p++) {
+      for (int n = 0; n < 4; n++) {
+        const bf16_t* vr = Vt + (n * 16 + c) * VTS + 32 * p + 4 * g;
+        dstv[n].u[0] = *(const uint2*)vr;
+        dstv[n].u[1] = *(const uint2*)(vr + 16);
+      }
+    };
+    load_v(0, vb[0]);
+#pragma unroll
+    for (int p = 0; p < NP; p++) {
       const int t0 = 2 * p, t1 = 2 * p + 1;
-      if (t0 < nkt) {
-        union { bf16_t u[8]; bf16x8_t v; } cv;
+      if (p + 1 < NP) load_v(p + 1, vb[(p + 1) & 1]);
+      union { uint32_t u[4]; bf16x8_t v; } cv;
+      cv.u[0] = pack_bf16x2(S[t0][0], S[t0][1]);
+      cv.u[1] = pack_bf16x2(S[t0][2], S[t0][3]);
+      if (t1 < MAXT) {
+        cv.u[2] = pack_bf16x2(S[t1 < MAXT ? t1 : 0][0], S[t1 < MAXT ? t1 : 0][1]);
+        cv.u[3] = pack_bf16x2(S[t1 < MAXT ? t1 : 0][2], S[t1 < MAXT ? t1 : 0][3]);
+      } else {
+        cv.u[2] = 0u;
+        cv.u[3] = 0u;
+      }
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-          cv.u[j] = f32_to_bf16(S[t0][j]);
-          cv.u[4 + j] = (t1 < MAXT) ? f32_to_bf16(S[t1 < MAXT ? t1 : 0][j]) : (bf16_t)0;
-        }
-        const int kl = 32 * p + 4 * g;
+      for (int n = 0; n < 4; n++)
+        O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[p & 1][n].v, cv.v, O[n], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const int q = q0 + c;
+    if (q < Tn) {
+      bf16_t* orow = out + (size_t)(base + q) * d + h * 64 + 4 * g;
 #pragma unroll
-        for (int n = 0; n < 4; n++) {
-          const bf16_t* vr = Vt + (n * 16 + c) * VTS + kl;
-          union { uint2 u[2]; bf16x8_t v; } vb;
-          vb.u[0] = *(const uint2*)vr;
-          vb.u[1] = *(const uint2*)(vr + 16);
-          O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cv.v, vb.v, O[n], 0, 0, 0);
-        }
+      for (int n = 0; n < 4; n++) {
+        *(uint2*)(orow + n * 16) = make_uint2(pack_bf16x2(O[n][0] * rl, O[n][1] * rl),
+                                              pack_bf16x2(O[n][2] * rl, O[n][3] * rl));
       }
     }
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const int q = q0 + 4 * g + j;
-      const float l = __shfl(rl, 4 * g + j, 64);
-      if (q < Tn) {
-#pragma unroll
-        for (int n = 0; n < 4; n++)
-          out[(size_t)(base + q) * d + h * 64 + n * 16 + c] = f32_to_bf16(O[n][j] * l);
-      }
-    }
+  }
+  // CLS-query probabilities of this head (prune blocks), copied out by the
+  // whole workgroup once wave 0 has written them
+  if (want_cls) {
+    __syncthreads();
+    float* cs = a.cls_scores + ((size_t)i * a.H + h) * a.tmax;
+    for (int k = tid; k < Tn; k += RES_NT) cs[k] = clsP[k];
   }
 }
 
@@ -488,12 +518,18 @@ template <typename T>
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
   if (sizeof(T) == 2 && a.dh == 64) {
-    if (a.T_ub <= 16 * 13) {
-      attention_mfma_res<13><<<dim3(a.nlive_ub, a.H), 256, 0, s>>>(a);
-      return hipGetLastError();
-    }
     if (a.T_ub <= 16 * 16) {
-      attention_mfma_res<16><<<dim3(a.nlive_ub, a.H), 256, 0, s>>>(a);
+      const dim3 grid(a.nlive_ub, a.H);
+      switch ((a.T_ub + 15) / 16) {
+#define FUSION_ATTN_RES(n) \
+  case n: attention_mfma_res<n><<<grid, RES_NT, 0, s>>>(a); break;
+        FUSION_ATTN_RES(1) FUSION_ATTN_RES(2) FUSION_ATTN_RES(3) FUSION_ATTN_RES(4)
+        FUSION_ATTN_RES(5) FUSION_ATTN_RES(6) FUSION_ATTN_RES(7) FUSION_ATTN_RES(8)
+        FUSION_ATTN_RES(9) FUSION_ATTN_RES(10) FUSION_ATTN_RES(11) FUSION_ATTN_RES(12)
+        FUSION_ATTN_RES(13) FUSION_ATTN_RES(14) FUSION_ATTN_RES(15) FUSION_ATTN_RES(16)
+#undef FUSION_ATTN_RES
+        default: return hipErrorInvalidValue;
+      }
       return hipGetLastError();
     }
     dim3 grid(a.nlive_ub, a.H, (a.T_ub + 63) / 64);

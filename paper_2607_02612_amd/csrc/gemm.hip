@@ -269,9 +269,7 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
           if (EPI == EPI_GELU) {
             v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
           }
-          uint2 pk;
-          pk.x = (uint32_t)f32_to_bf16(v0) | ((uint32_t)f32_to_bf16(v1) << 16);
-          pk.y = (uint32_t)f32_to_bf16(v2) | ((uint32_t)f32_to_bf16(v3) << 16);
+          const uint2 pk = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
           *(uint2*)(smem + r * (NB * 2) + (((c >> 3) ^ (r & 15)) << 4) + ((c >> 2) & 1) * 8) = pk;
         }
       }

@@ -62,10 +62,7 @@ template <> struct Vec4<float> {
 };
 template <> struct Vec4<bf16_t> {
   static __device__ __forceinline__ void put(bf16_t* d, float4 v) {
-    uint2 u;
-    u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
-    u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
-    *(uint2*)d = u;
+    *(uint2*)d = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
   }
 };
 
