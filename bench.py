@@ -56,13 +56,15 @@ def kernel_work(cfg, counts):
         "gemm_fc2": ("flop", float((2 * M * mlp * d).sum())),
         "attention": ("flop", float((4 * T * T * d).sum())),
         "patch_embed": ("flop", 2.0 * counts.shape[0] * cfg["N0"] * cfg["patch_dim"] * d),
-        # LayerNorm: read fp32 rows, write bf16 rows, twice per block
-        "layernorm": ("byte", float((2 * M * d * (4 + 2)).sum())),
+        # LayerNorm kernel: read fp32 rows, write bf16 rows; LN2 of every
+        # block and LN1 of block 1 (later LN1s are written by the compaction)
+        "layernorm": ("byte", float((M * d * (4 + 2)).sum() + M[0] * d * (4 + 2))),
     }
     # adapt: read the sample's fp32 rows and sizes, write the merged rows
-    # back; compaction: read and write the kept rows (x, size, origin)
+    # back; compaction after block b: read and write the rows kept for block
+    # b + 1 (x, size, origin) and write their LN1 (bf16)
     w["adapt"] = ("byte", float((M * (d * 4 + 8) * 2).sum()))
-    w["compact"] = ("byte", float((M * (d * 4 + 8) * 2).sum()))
+    w["compact"] = ("byte", float((M[1:] * ((d * 4 + 8) * 2 + d * 2)).sum()))
     return w
 
 

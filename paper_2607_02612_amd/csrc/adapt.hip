@@ -427,12 +427,16 @@ hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
 }
 
 // --------------------------------------------------------- compaction --
+// Grid: (live sample, part); every workgroup of a sample recomputes the
+// sample's offsets (cheap scans) and moves one contiguous range of its rows.
+constexpr int CP_PARTS = 4;
+template <typename T>
 __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
-  const int i = blockIdx.x;
+  const int i = blockIdx.x, part = blockIdx.y;
   const int nl = a.cnt->nlive;
-  // Workgroup 0 always publishes the next counters, also when no sample is
-  // live any more (the next block must see nlive = 0, not a stale value).
-  if (i >= nl && i != 0) return;
+  // Workgroup (0, 0) always publishes the next counters, also when no sample
+  // is live any more (the next block must see nlive = 0, not a stale value).
+  if (i >= nl && (i != 0 || part != 0)) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   __shared__ int ired[8];
   __shared__ int dsts[AD_TMAX];
@@ -446,7 +450,7 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   }
   off = block_sum256_i(off, ired);
   j = block_sum256_i(j, ired);
-  if (i == 0) {
+  if (i == 0 && part == 0) {
     int tot = 0, nn = 0;
     for (int t = tid; t < nl; t += 256) {
       const int n = a.newlen[t];
@@ -462,16 +466,16 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
     }
   }
   if (i >= nl || a.newlen[i] == 0) return;
-  const int base = a.cu[i], T = a.cu[i + 1] - base;
+  const int base = a.cu[i], Tn = a.cu[i + 1] - base;
   const int orig = a.live[i];
-  if (tid == 0) {
+  if (tid == 0 && part == 0) {
     a.cu2[j] = off;
     a.live2[j] = orig;
   }
-  const int nch = (T + 63) / 64;
+  const int nch = (Tn + 63) / 64;
   for (int c = wave; c < nch; c += 4) {
     const int t = c * 64 + lane;
-    const unsigned long long msk = __ballot(t < T && a.keep[base + t]);
+    const unsigned long long msk = __ballot(t < Tn && a.keep[base + t]);
     if (lane == 0) chunk_off[c] = __popcll(msk);
   }
   __syncthreads();
@@ -486,20 +490,25 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   __syncthreads();
   for (int c = wave; c < nch; c += 4) {
     const int t = c * 64 + lane;
-    const bool f = t < T && a.keep[base + t];
+    const bool f = t < Tn && a.keep[base + t];
     const unsigned long long msk = __ballot(f);
     const int pos = __popcll(msk & ((1ull << lane) - 1ull));
-    if (t < T) dsts[t] = f ? chunk_off[c] + pos : -1;
+    if (t < Tn) dsts[t] = f ? chunk_off[c] + pos : -1;
   }
   __syncthreads();
-  const int d4 = a.d / 4;
-  for (int idx = tid; idx < T * d4; idx += 256) {
-    const int t = idx / d4, f = idx - t * d4;
+  // kept rows of this part (the sample's rows split into CP_PARTS ranges):
+  // one half wave per row copies it (16-byte pieces) and, when asked,
+  // writes its LayerNorm for the next block
+  const int per = (Tn + CP_PARTS - 1) / CP_PARTS;
+  const int t0 = part * per, t1 = min(Tn, t0 + per);
+  for (int t = t0 + (tid >> 5); t < t1; t += 8) {
     const int dj = dsts[t];
-    if (dj >= 0)
-      ((float4*)a.x2)[(size_t)(off + dj) * d4 + f] = ((const float4*)a.x)[(size_t)(base + t) * d4 + f];
+    if (dj < 0) continue;
+    const size_t dr = (size_t)(off + dj);
+    ln_row_half<T>(a.x + (size_t)(base + t) * a.d, a.d, lane & 31, a.ln_g, a.ln_b,
+                   a.ln_out ? (T*)a.ln_out + dr * a.d : nullptr, a.x2 + dr * a.d);
   }
-  for (int t = tid; t < T; t += 256) {
+  for (int t = t0 + tid; t < t1; t += 256) {
     const int dj = dsts[t];
     if (dj < 0) continue;
     a.size2[off + dj] = a.size[base + t];
@@ -509,11 +518,14 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   }
 }
 
+template <typename T>
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
-  if (a.n0 + 1 > AD_TMAX || a.d % 4 != 0) return hipErrorInvalidValue;
-  compact_kernel<<<a.nlive_ub, 256, 0, s>>>(a);
+  if (a.n0 + 1 > AD_TMAX || a.d % 4 != 0 || a.d > 4 * 32 * LN_MAXV) return hipErrorInvalidValue;
+  compact_kernel<T><<<dim3(a.nlive_ub, CP_PARTS), 256, 0, s>>>(a);
   return hipGetLastError();
 }
+template hipError_t launch_compact<float>(const CompactArgs&, hipStream_t);
+template hipError_t launch_compact<bf16_t>(const CompactArgs&, hipStream_t);
 
 }  // namespace fusion

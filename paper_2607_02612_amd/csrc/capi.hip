@@ -355,17 +355,19 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
   const double tau_rho = m->rho;
   int T_ub = T0;
   const fusion_trace* tr = o.trace;
+  bool ln1_done = false;  // act already holds this block's LN1 (from the compaction)
   for (int b = 1; b <= L; b++) {
     const BlockW& w = m->blk[b - 1];
     const bool isM = c.merge_mask >> (b - 1) & 1, isE = c.exit_mask >> (b - 1) & 1,
                isP = c.prune_mask >> (b - 1) & 1;
     const int M_ub = B * T_ub;
     const int* Mdev = &m->cnt[cur]->M;
-    {
+    if (!ln1_done) {
       Prof p(m, s, K_LN);
       HIP_OR_FAIL(launch_layernorm<T>(m->x[cur], w.ln1_g, w.ln1_b, (T*)m->act, d, m->cnt[cur],
                                       m->cu[cur], m->live[cur], 0, M_ub, nullptr, L, s));
     }
+    ln1_done = false;
     {
       Prof p(m, s, K_QKV);
       Epi e{EPI_STORE, m->qkv, 3 * d, w.qkv_b, nullptr, nullptr, 0};
@@ -446,7 +448,14 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
         a.live2 = m->live[nx]; a.cnt2 = m->cnt[nx];
         a.d = d; a.n0 = n0; a.B = B; a.b = b; a.tr_ids = tr ? tr->ids : nullptr;
         a.nlive_ub = B;
-        HIP_OR_FAIL(launch_compact(a, s));
+        // the moved rows are the next block's input: write its LN1 on the way
+        if (b < L) {
+          a.ln_g = m->blk[b].ln1_g;
+          a.ln_b = m->blk[b].ln1_b;
+          a.ln_out = m->act;
+        }
+        HIP_OR_FAIL(launch_compact<T>(a, s));
+        ln1_done = b < L;
         cur = nx;
       }
       if (isP) {

@@ -106,6 +106,77 @@ __device__ __forceinline__ int block_sum256_i(int v, int* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
+// Sum over the 32 lanes of a half wave (lanes 0-31 or 32-63).
+__device__ __forceinline__ float half_sum(float v) {
+#pragma unroll
+  for (int o = 16; o > 0; o >>= 1) v += __shfl_xor(v, o, 32);
+  return v;
+}
+
+// Four floats -> storage type, one vector store.
+template <typename T> struct Store4;
+template <> struct Store4<float> {
+  static __device__ __forceinline__ void put(float* p, float4 v) { *(float4*)p = v; }
+};
+template <> struct Store4<bf16_t> {
+  static __device__ __forceinline__ void put(bf16_t* p, float4 v) {
+    *(uint2*)p = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+  }
+};
+
+// LayerNorm of one row of d fp32 values by a half wave (l = lane % 32 holds
+// the 16-byte pieces l, l + 32, ...; d % 4 == 0, d <= 768): mean and biased
+// variance in fp32 (two passes over the values held in registers),
+// y = (x - mean) / sqrt(var + 1e-6) * g + b.  Optionally copies the row to
+// `copy` on the way.
+constexpr int LN_MAXV = 6;  // 16-byte pieces per lane (d <= 768)
+template <typename T>
+__device__ __forceinline__ void ln_row_half(const float* __restrict__ xr, int d, int l,
+                                            const float* __restrict__ g,
+                                            const float* __restrict__ b, T* __restrict__ out,
+                                            float* __restrict__ copy) {
+  const int n4 = d >> 2;
+  float4 v[LN_MAXV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; i++) {
+    const int k = l + 32 * i;
+    v[i] = k < n4 ? ((const float4*)xr)[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+    s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+  }
+  if (copy) {
+#pragma unroll
+    for (int i = 0; i < LN_MAXV; i++) {
+      const int k = l + 32 * i;
+      if (k < n4) ((float4*)copy)[k] = v[i];
+    }
+  }
+  if (!out) return;
+  const float mean = half_sum(s) / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; i++) {
+    const int k = l + 32 * i;
+    if (k < n4) {
+      const float a0 = v[i].x - mean, a1 = v[i].y - mean, a2 = v[i].z - mean, a3 = v[i].w - mean;
+      q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+    }
+  }
+  const float var = half_sum(q) / (float)d;
+  const float rstd = 1.0f / sqrtf(var + 1e-6f);
+#pragma unroll
+  for (int i = 0; i < LN_MAXV; i++) {
+    const int k = l + 32 * i;
+    if (k < n4) {
+      const float4 gg = ((const float4*)g)[k], bb = ((const float4*)b)[k];
+      Store4<T>::put(out + 4 * k, make_float4(((v[i].x - mean) * rstd) * gg.x + bb.x,
+                                              ((v[i].y - mean) * rstd) * gg.y + bb.y,
+                                              ((v[i].z - mean) * rstd) * gg.z + bb.z,
+                                              ((v[i].w - mean) * rstd) * gg.w + bb.w));
+    }
+  }
+}
+
 // erf by the rational approximation 7.1.26 of Abramowitz & Stegun
 // (Handbook of Mathematical Functions): for x >= 0,
 //   erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2),

@@ -121,7 +121,13 @@ struct CompactArgs {
   int d, n0, B, b;
   int* tr_ids;
   int nlive_ub;
+  // optional: LayerNorm of every moved row with (ln_g, ln_b) into ln_out
+  // (storage type T of the precision path), i.e. the next block's LN1
+  const float* ln_g;
+  const float* ln_b;
+  void* ln_out;
 };
+template <typename T>
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 
 // Copy of the packed state for diagnostics.

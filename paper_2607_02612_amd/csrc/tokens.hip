@@ -56,16 +56,6 @@ hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
 // of a kernel row (p % 4 == 0): a 16-byte load and one vector store, with
 // consecutive threads on consecutive pixels; 32-bit index math (the host
 // checks that B * n0 * C * p * p / 4 fits).
-template <typename T> struct Vec4;
-template <> struct Vec4<float> {
-  static __device__ __forceinline__ void put(float* d, float4 v) { *(float4*)d = v; }
-};
-template <> struct Vec4<bf16_t> {
-  static __device__ __forceinline__ void put(bf16_t* d, float4 v) {
-    *(uint2*)d = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
-  }
-};
-
 template <typename T>
 __global__ void patchify_kernel(const float* __restrict__ img, T* __restrict__ out,
                                 int B, int C, int S, int p) {
@@ -79,7 +69,7 @@ __global__ void patchify_kernel(const float* __restrict__ img, T* __restrict__ o
     const int s = row / n0, j = row - s * n0;
     const int gy = j / g, gx = j - gy * g;
     const float4 v = *(const float4*)(img + (((size_t)s * C + c) * S + gy * p + ky) * S + gx * p + kx);
-    Vec4<T>::put(out + (size_t)row * pd + e, v);
+    Store4<T>::put(out + (size_t)row * pd + e, v);
   }
 }
 
@@ -96,46 +86,21 @@ hipError_t launch_patchify(const float* img, T* out, int B, int C, int S,
 template hipError_t launch_patchify<float>(const float*, float*, int, int, int, int, hipStream_t);
 template hipError_t launch_patchify<bf16_t>(const float*, bf16_t*, int, int, int, int, hipStream_t);
 
-// One wave per row: mean and biased variance in fp32 (two passes over the
-// row held in registers), y = (x - mean) / sqrt(var + 1e-6) * g + b.
+// One half wave per row (8 rows per 256-thread workgroup), 16-byte loads and
+// vector stores; the row arithmetic is ln_row_half.
 template <typename T>
 __global__ __launch_bounds__(256) void layernorm_kernel(
     const float* __restrict__ x, const float* __restrict__ g,
     const float* __restrict__ bb, T* __restrict__ out, int d,
     const LiveCounts* cnt, const int* __restrict__ cu,
     const int* __restrict__ live, int cls_only, int* exit_block, int L) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + wave;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
   const int nrows = cls_only ? cnt->nlive : cnt->M;
   if (row >= nrows) return;
   const size_t src = cls_only ? (size_t)cu[row] : (size_t)row;
-  const float* xr = x + src * d;
-  constexpr int MAXV = 12;  // d <= 768
-  float v[MAXV];
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < MAXV; i++) {
-    const int n = lane + i * 64;
-    v[i] = n < d ? xr[n] : 0.f;
-    s += v[i];
-  }
-  const float mean = wave_sum(s) / (float)d;
-  float q = 0.f;
-#pragma unroll
-  for (int i = 0; i < MAXV; i++) {
-    const int n = lane + i * 64;
-    const float c = n < d ? v[i] - mean : 0.f;
-    q += c * c;
-  }
-  const float var = wave_sum(q) / (float)d;
-  const float rstd = 1.0f / sqrtf(var + 1e-6f);
-  T* o = out + (size_t)row * d;
-#pragma unroll
-  for (int i = 0; i < MAXV; i++) {
-    const int n = lane + i * 64;
-    if (n < d) o[n] = St<T>::put(((v[i] - mean) * rstd) * g[n] + bb[n]);
-  }
-  if (exit_block && lane == 0) exit_block[live[row]] = L;
+  ln_row_half<T>(x + src * d, d, lane & 31, g, bb, out + (size_t)row * d, nullptr);
+  if (exit_block && (lane & 31) == 0) exit_block[live[row]] = L;
 }
 
 template <typename T>
@@ -145,8 +110,8 @@ hipError_t launch_layernorm(const float* x, const float* g, const float* b,
                             int rows_ub, int* exit_block, int L,
                             hipStream_t s) {
   if (rows_ub <= 0) return hipSuccess;
-  if (d > 768) return hipErrorInvalidValue;
-  layernorm_kernel<T><<<(rows_ub + 3) / 4, 256, 0, s>>>(
+  if (d > 4 * 32 * LN_MAXV || d % 4 != 0) return hipErrorInvalidValue;
+  layernorm_kernel<T><<<(rows_ub + 7) / 8, 256, 0, s>>>(
       x, g, b, out, d, cnt, cu, live, cls_only, exit_block, L);
   return hipGetLastError();
 }
