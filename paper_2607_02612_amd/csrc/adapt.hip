@@ -12,14 +12,23 @@
 
 namespace fusion {
 
-constexpr int AD_TMAX = 640;  // tokens per sample (CLS included)
-constexpr int AD_AMAX = 320;  // |A| = ceil(N/2)
-constexpr int AD_BMAX = 320;  // |B| = floor(N/2)
+constexpr int AD_TMAX = 640;  // tokens per sample (CLS included), largest size class
 constexpr int AD_NT = 512;    // threads per workgroup (8 waves)
-constexpr int SKC = 32;       // feature chunk of the similarity MFMAs
-constexpr int SKP = SKC + 8;  // padded LDS row (bf16)
 constexpr int SAG = 128;      // A rows per pass: one 16-row MFMA tile per wave
-constexpr int SNBT = AD_BMAX / 16;  // B tiles held in registers
+
+// Size classes of the per-sample kernel: TMAX tokens (CLS included), so
+// |A| = ceil(N/2) and |B| = floor(N/2) are at most TMAX/2; the similarity
+// features are staged in chunks of SKC (64 for the small class: fewer
+// round trips to memory; 32 for the large one, whose B tiles fill the LDS).
+template <int TMAX_> struct AdSize {
+  static constexpr int TMAX = TMAX_;
+  static constexpr int AMAX = TMAX_ / 2;
+  static constexpr int BMAX = TMAX_ / 2;
+  static constexpr int SKC = TMAX_ <= 256 ? 64 : 32;
+  static constexpr int SKP = SKC + 8;          // padded LDS row (bf16)
+  static constexpr int NBT = BMAX / 16;        // B tiles held in registers
+  static constexpr int SPT = ((SAG + BMAX) * (SKC / 4) + AD_NT - 1) / AD_NT;  // slots / thread
+};
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -106,12 +115,12 @@ __device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
 // max(||x||, 1e-12) of both tokens.  Wave w owns A rows ag + 16w .. +15
 // against every B tile; lane l of an output tile holds S[a = 4(l/16) + j]
 // [b = l%16].
-constexpr int SPT = ((SAG + AD_BMAX) * (SKC / 4) + AD_NT - 1) / AD_NT;  // slots / thread
-
+template <class Z>
 __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
                                   int nA, int nB, float* nrm, float* bestsim,
                                   int* best, bf16_t* Ahi, bf16_t* Alo,
                                   bf16_t* Bhi, bf16_t* Blo) {
+  constexpr int SKC = Z::SKC, SKP = Z::SKP, SPT = Z::SPT, NBT = Z::NBT;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c = lane & 15;
   const int nbt = (nB + 15) >> 4;
@@ -138,9 +147,9 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
 #pragma unroll
     for (int w = 0; w < SPT; w++)
       cur[w] = srow[w] ? *(const float4*)srow[w] : make_float4(0.f, 0.f, 0.f, 0.f);
-    f32x4_t acc[SNBT];
+    f32x4_t acc[NBT];
 #pragma unroll
-    for (int t = 0; t < SNBT; t++) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < NBT; t++) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int k0 = 0; k0 < d; k0 += SKC) {
       __syncthreads();
 #pragma unroll
@@ -150,12 +159,19 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
         const int r = u / (SKC / 4), q = (u % (SKC / 4)) * 4;
         bf16_t* H = r < SAG ? Ahi + r * SKP : Bhi + (r - SAG) * SKP;
         bf16_t* Lo = r < SAG ? Alo + r * SKP : Blo + (r - SAG) * SKP;
-        const float e[4] = {cur[w].x, cur[w].y, cur[w].z, cur[w].w};
-#pragma unroll
-        for (int z = 0; z < 4; z++) {
-          ss[w] = fmaf(e[z], e[z], ss[w]);
-          split_bf16(e[z], H[q + z], Lo[q + z]);
-        }
+        const float4 e = cur[w];
+        ss[w] = fmaf(e.x, e.x, ss[w]);
+        ss[w] = fmaf(e.y, e.y, ss[w]);
+        ss[w] = fmaf(e.z, e.z, ss[w]);
+        ss[w] = fmaf(e.w, e.w, ss[w]);
+        // hi = RNE(v), lo = RNE(v - hi): four values -> two 8-byte stores
+        const uint32_t h01 = pack_bf16x2(e.x, e.y), h23 = pack_bf16x2(e.z, e.w);
+        const uint32_t l01 = pack_bf16x2(e.x - __uint_as_float(h01 << 16),
+                                         e.y - __uint_as_float(h01 & 0xFFFF0000u));
+        const uint32_t l23 = pack_bf16x2(e.z - __uint_as_float(h23 << 16),
+                                         e.w - __uint_as_float(h23 & 0xFFFF0000u));
+        *(uint2*)(H + q) = make_uint2(h01, h23);
+        *(uint2*)(Lo + q) = make_uint2(l01, l23);
       }
       // prefetch the next chunk while this one is multiplied
       if (k0 + SKC < d) {
@@ -164,16 +180,21 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
           if (srow[w]) cur[w] = *(const float4*)(srow[w] + k0 + SKC);
       }
       __syncthreads();
-      const bf16x8_t ah = *(const bf16x8_t*)(Ahi + (wave * 16 + c) * SKP + 8 * g);
-      const bf16x8_t al = *(const bf16x8_t*)(Alo + (wave * 16 + c) * SKP + 8 * g);
+      // 32 features per MFMA; per B tile the products accumulate in feature
+      // order, hi.hi' then hi.lo' then lo.hi' within each 32
 #pragma unroll
-      for (int t = 0; t < SNBT; t++) {
-        if (t < nbt) {
-          const bf16x8_t bh = *(const bf16x8_t*)(Bhi + (t * 16 + c) * SKP + 8 * g);
-          const bf16x8_t bl = *(const bf16x8_t*)(Blo + (t * 16 + c) * SKP + 8 * g);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc[t], 0, 0, 0);
-          acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc[t], 0, 0, 0);
+      for (int kk = 0; kk < SKC / 32; kk++) {
+        const bf16x8_t ah = *(const bf16x8_t*)(Ahi + (wave * 16 + c) * SKP + 32 * kk + 8 * g);
+        const bf16x8_t al = *(const bf16x8_t*)(Alo + (wave * 16 + c) * SKP + 32 * kk + 8 * g);
+#pragma unroll
+        for (int t = 0; t < NBT; t++) {
+          if (t < nbt) {
+            const bf16x8_t bh = *(const bf16x8_t*)(Bhi + (t * 16 + c) * SKP + 32 * kk + 8 * g);
+            const bf16x8_t bl = *(const bf16x8_t*)(Blo + (t * 16 + c) * SKP + 32 * kk + 8 * g);
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc[t], 0, 0, 0);
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc[t], 0, 0, 0);
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc[t], 0, 0, 0);
+          }
         }
       }
     }
@@ -199,7 +220,7 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
       float bv = -INFINITY;
       int bi = 0x7fffffff;
 #pragma unroll
-      for (int t = 0; t < SNBT; t++) {
+      for (int t = 0; t < NBT; t++) {
         const int bb = t * 16 + c;
         if (t < nbt && bb < nB) {
           const float v = acc[t][j] / (na * nrm[2 * bb + 1]);
@@ -227,6 +248,7 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
   }
 }
 
+template <class Z>
 __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   const int i = blockIdx.x;
   if (i >= a.cnt->nlive) return;
@@ -236,22 +258,23 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   const int d = a.d;
   const size_t tr_row = (size_t)(a.b - 1) * a.B + orig;
 
-  __shared__ float sc[AD_TMAX];
-  __shared__ float szs[AD_TMAX];
-  __shared__ int keepf[AD_TMAX];
-  __shared__ float nrm[AD_TMAX];
-  __shared__ float bestsim[AD_AMAX];
-  __shared__ int best[AD_AMAX];
-  __shared__ int chosen[AD_AMAX];
-  __shared__ int clist[AD_AMAX];
-  __shared__ int cdst[AD_AMAX];
-  __shared__ int glead[AD_AMAX];
-  __shared__ float tmpf[AD_AMAX];
-  __shared__ float tmps[AD_AMAX];
+  constexpr int TMAX = Z::TMAX, AMAX = Z::AMAX, BMAX = Z::BMAX, SKP = Z::SKP;
+  __shared__ float sc[TMAX];
+  __shared__ float szs[TMAX];
+  __shared__ int keepf[TMAX];
+  __shared__ float nrm[TMAX];
+  __shared__ float bestsim[AMAX];
+  __shared__ int best[AMAX];
+  __shared__ int chosen[AMAX];
+  __shared__ int clist[AMAX];
+  __shared__ int cdst[AMAX];
+  __shared__ int glead[AMAX];
+  __shared__ float tmpf[AMAX];
+  __shared__ float tmps[AMAX];
   __shared__ __attribute__((aligned(16))) bf16_t Ahi[SAG * SKP];
   __shared__ __attribute__((aligned(16))) bf16_t Alo[SAG * SKP];
-  __shared__ __attribute__((aligned(16))) bf16_t Bhi[AD_BMAX * SKP];
-  __shared__ __attribute__((aligned(16))) bf16_t Blo[AD_BMAX * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bhi[BMAX * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Blo[BMAX * SKP];
   __shared__ float red[16];
   __shared__ int ired[16];
 
@@ -283,7 +306,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   }
   const int nA = (N + 1) / 2, nB = N / 2;
   if (r > 0) {
-    similarity_argmax(a.x, base, d, nA, nB, nrm, bestsim, best, Ahi, Alo, Bhi, Blo);
+    similarity_argmax<Z>(a.x, base, d, nA, nB, nrm, bestsim, best, Ahi, Alo, Bhi, Blo);
     // top-r of A by best similarity, ties to the lower A slot
     for (int aa = tid; aa < nA; aa += AD_NT) {
       const float v = bestsim[aa];
@@ -386,7 +409,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     for (int t = 1 + tid; t < T; t += AD_NT) ns += keepf[t];
     ns = bsum_i(ns, ired);
     const int k = (int)floor(__dmul_rn(a.tau_eff, (double)ns));
-    constexpr int U = (AD_TMAX + AD_NT - 1) / AD_NT;
+    constexpr int U = (TMAX + AD_NT - 1) / AD_NT;
     int keep_new[U];
 #pragma unroll
     for (int u = 0; u < U; u++) {
@@ -421,8 +444,13 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
 
 hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
-  if (a.n0 + 1 > AD_TMAX || a.d % SKC != 0) return hipErrorInvalidValue;
-  adapt_kernel<<<a.nlive_ub, AD_NT, 0, s>>>(a);
+  if (a.n0 + 1 <= 256) {
+    if (a.d % AdSize<256>::SKC != 0) return hipErrorInvalidValue;
+    adapt_kernel<AdSize<256>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
+  } else {
+    if (a.n0 + 1 > AD_TMAX || a.d % AdSize<AD_TMAX>::SKC != 0) return hipErrorInvalidValue;
+    adapt_kernel<AdSize<AD_TMAX>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
+  }
   return hipGetLastError();
 }
 
