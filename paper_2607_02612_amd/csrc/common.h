@@ -177,26 +177,23 @@ __device__ __forceinline__ void ln_row_half(const float* __restrict__ xr, int d,
   }
 }
 
-// erf by the rational approximation 7.1.26 of Abramowitz & Stegun
-// (Handbook of Mathematical Functions): for x >= 0,
-//   erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2),
-//   t = 1 / (1 + p x),
-// absolute error <= 1.5e-7 (plus fp32 rounding); odd in x.
-__device__ __forceinline__ float erf_as7126(float x) {
-  const float ax = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
-  float y = fmaf(t, 1.061405429f, -1.453152027f);
-  y = fmaf(t, y, 1.421413741f);
-  y = fmaf(t, y, -0.284496736f);
-  y = fmaf(t, y, 0.254829592f);
-  const float e = __builtin_amdgcn_exp2f(-(ax * ax) * 1.4426950408889634f);
-  const float r = fmaf(-(t * y), e, 1.0f);
-  return copysignf(r, x);
-}
-
-// GELU with the exact (erf) form, 0.5 v (1 + erf(v / sqrt 2)).
+// GELU with the exact (erf) form, v Phi(v), Phi the standard normal CDF,
+// written as GELU(v) = max(v, 0) - |v| Q(|v|) with the upper tail
+// Q(a) = erfc(a / sqrt 2) / 2 from the rational approximation 7.1.26 of
+// Abramowitz & Stegun (Handbook of Mathematical Functions):
+//   erfc(z) = t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-z^2),
+//   t = 1 / (1 + p z), |error| <= 1.5e-7,
+// with z = a / sqrt 2 folded into p and into the exponent and the 1/2 into
+// a1..a5.  The tail form has no cancellation for negative v.
 __device__ __forceinline__ float gelu_erf(float v) {
-  return 0.5f * v * (1.0f + erf_as7126(v * 0.70710678118654752f));
+  const float a = fabsf(v);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, a, 1.0f));
+  float y = fmaf(t, 0.5f * 1.061405429f, 0.5f * -1.453152027f);
+  y = fmaf(t, y, 0.5f * 1.421413741f);
+  y = fmaf(t, y, 0.5f * -0.284496736f);
+  y = fmaf(t, y, 0.5f * 0.254829592f);
+  const float e = __builtin_amdgcn_exp2f(v * (v * (-0.5f * 1.4426950408889634f)));
+  return fmaf(-a, (t * y) * e, fmaxf(v, 0.f));
 }
 
 }  // namespace fusion

@@ -98,8 +98,8 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 }
 
 // ------------------------------------------------------------ bf16 MFMA --
-// MBx128 output tile per workgroup (MB = 128: 4 waves in a 2x2 grid; MB =
-// 64: 2 waves side by side), each wave a 64x64 sub-tile of 2x2
+// MBx128 output tile per workgroup (MB = 256: 8 waves in a 4x2 grid; 128: 4
+// waves, 2x2; 64: 2 waves side by side), each wave a 64x64 sub-tile of 2x2
 // v_mfma_f32_32x32x16_bf16 blocks.
 //
 // K is consumed in steps of KSV = 32 (three LDS stages) or 64 (two stages,
@@ -133,6 +133,10 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 constexpr int NB = 128;
 constexpr int NXCD = 8;
 
+#ifndef GEMM_BIG_TILES
+#define GEMM_BIG_TILES 1
+#endif
+
 template <int KSV>
 __device__ __forceinline__ int kslot(int r, int c) {
   return KSV == 32 ? (c ^ ((r >> 2) & 3)) : (c ^ ((r >> 1) & 7));
@@ -147,8 +151,8 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
-// MB = 128 (4 waves, 2x2) or 64 (2 waves, 1x2) rows per tile; the smaller
-// tile is chosen when 128-row tiles would leave CUs idle.  KSV = K step.
+// MB = 256 (8 waves, 4x2), 128 (4 waves, 2x2) or 64 (2 waves, 1x2) rows per
+// tile.  KSV = K step.
 template <int EPI, int MB, int KSV>
 __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
@@ -350,18 +354,23 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   if ((e.mode == EPI_STORE || e.mode == EPI_GELU) && (N % 8 != 0 || e.ldo % 8 != 0))
     return hipErrorInvalidValue;
   const int n_nt = (N + NB - 1) / NB;
+  // tile rows: 256 (8 waves) when there are enough tiles to fill the CUs
+  // several times over, 64 when 128-row tiles would leave CUs idle
   const bool small = (long)((M_ub + 127) / 128) * n_nt < 512;
-  const int mb = small ? 64 : 128;
+  // long K on 128-row tiles: 64-wide K steps (half the barriers); otherwise
+  // 32-wide steps with three stages
+  const bool k64 = !small && K % 64 == 0 && K >= 1024;
+  const bool big = !k64 && GEMM_BIG_TILES && (long)((M_ub + 255) / 256) * n_nt >= 1024;
+  const int mb = small ? 64 : big ? 256 : 128;
   const int n_mt = (M_ub + mb - 1) / mb;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
-  // long K on 128-row tiles: 64-wide K steps (half the barriers); otherwise
-  // 32-wide steps with three stages (three workgroups per CU)
-  const bool k64 = !small && K % 64 == 0 && K >= 1024;
 #define FUSION_GEMM_LAUNCH(E)                                                                 \
   if (small)                                                                                 \
     gemm_mfma_bf16<E, 64, 32><<<grid, 128, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
   else if (k64)                                                                              \
     gemm_mfma_bf16<E, 128, 64><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
+  else if (big)                                                                              \
+    gemm_mfma_bf16<E, 256, 32><<<grid, 512, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
   else                                                                                       \
     gemm_mfma_bf16<E, 128, 32><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e)
   switch (e.mode) {
