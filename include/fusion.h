@@ -42,6 +42,26 @@ typedef enum fusion_status {
   FUSION_E_STATE = -6        /* call not valid in the model's state */
 } fusion_status;
 
+/* Merge-count rules (Sec. III-C, Eq. 4-5), with m the router output and
+ * rho the router strength (fusion_set_router_strength):
+ *   BUDGET:   r = clamp(floor(2 rho m r_b + 1/2), 0, floor(N/2));
+ *   FRACTION: r = min(floor(((rho m) N) / 2), floor(N/2)), the merge ratio
+ *             m~ = rho m applied to the N/2 candidate pairs. */
+enum { FUSION_MERGE_BUDGET = 0, FUSION_MERGE_FRACTION = 1 };
+/* Token scores of the prune step (Eq. 8):
+ *   CLS_ATTN: head-mean CLS-attention probability of the block (added up
+ *             over merged tokens);
+ *   LEARNED:  s_i = w . z_i + beta, a linear scorer on the hidden states
+ *             after the block's merge (tensors prune_w [d], prune_b [1]). */
+enum { FUSION_PRUNE_CLS_ATTN = 0, FUSION_PRUNE_LEARNED = 1 };
+/* Exit-head kinds (Eq. 6 head_b; Sec. IV describes MLP heads):
+ *   LINEAR:   LN + linear on the CLS token;
+ *   CLS_MLP:  LN, linear to exit_hidden, exact GELU, linear to C, on CLS;
+ *   POOL_MLP: the same MLP on sum_t s_t z_t / sum_t s_t over the patch
+ *             tokens (token sizes s_t, CLS excluded; zero vector when no
+ *             patch token is left). */
+enum { FUSION_EXIT_LINEAR = 0, FUSION_EXIT_CLS_MLP = 1, FUSION_EXIT_POOL_MLP = 2 };
+
 /* Static description of a model (filled by fusion_model_info or
  * fusion_blob_inspect). */
 typedef struct fusion_info {
@@ -59,6 +79,10 @@ typedef struct fusion_info {
   double tau_b[FUSION_MAX_LAYERS];        /* keep ratio per block */
   float delta[FUSION_MAX_LAYERS];         /* current threshold per exit head */
   double rho;                             /* current router strength */
+  int32_t merge_rule;                     /* FUSION_MERGE_* */
+  int32_t prune_rule;                     /* FUSION_PRUNE_* */
+  int32_t exit_kind[FUSION_MAX_LAYERS];   /* FUSION_EXIT_* per block (exit blocks) */
+  int32_t exit_hidden;                    /* hidden width of MLP exit heads, 0 if none */
 } fusion_info;
 
 /* Per-block decision record written by fusion_run_traced.  Every pointer is
@@ -119,7 +143,7 @@ FUSION_API int fusion_set_exit_thresholds(fusion_model* m, const float* delta,
                                           int n_exit);
 
 /* Router strength rho: the profile ratio of Eq. 5.  Merge blocks merge
- * r = clamp(floor(2 rho m r_b + 1/2), 0, floor(N/2)) pairs; prune blocks
+ * r pairs by the model's merge rule (FUSION_MERGE_*); prune blocks
  * keep floor(tau' N) patch tokens with tau' = min(1, max(0, 1 - rho (1 -
  * tau_b))).  rho = 1 is the reference profile, rho = 0 disables merging and
  * pruning.  Range [0, 16].  Errors: FUSION_E_INVALID_ARG. */

@@ -32,22 +32,34 @@ Readings of the paper where it is silent (each also listed in the design doc):
       argmax ties -> lowest B slot; top-r by best similarity, ties -> lowest
       A slot; dst <- (s_dst x_dst + sum_asc s_a x_a) / (s_dst + sum_asc s_a);
       sizes and CLS scores add; survivors keep their order (Sec. III-C).
-  merge count: r = clamp(floor(2 rho m r_b + 1/2), 0, floor(N/2)) with
-      m = sigmoid(w . z_cls + beta) (Eq. 4); rho is the profile ratio of
-      Eq. 5 and 2 r_b replaces the candidate count N_b/2, so that a neutral
-      router (m = 1/2) merges exactly rho * r_b pairs.
-  exit: head_b = LN + linear on the CLS token, c = max softmax
+  merge count, rule "budget": r = clamp(floor(2 rho m r_b + 1/2), 0,
+      floor(N/2)) with m = sigmoid(w . z_cls + beta) (Eq. 4); rho is the
+      profile ratio of Eq. 5 and 2 r_b replaces the candidate count N_b/2,
+      so that a neutral router (m = 1/2) merges exactly rho * r_b pairs.
+  merge count, rule "fraction" (Sec. III-C as written): m~ = rho m (Eq. 5),
+      r = min(floor(m~ N / 2), floor(N/2)), the doubles formed in the order
+      ((rho m) N) / 2.
+  exit heads (kind per exit block): "linear" = LN + linear on the CLS
+      token; "cls_mlp" = LN, linear to the hidden width, exact GELU, linear
+      to C, on the CLS token; "pool_mlp" = the same MLP on the size-weighted
+      mean of the patch tokens sum_t s_t z_t / sum_t s_t (CLS excluded; a
+      sample without patch tokens pools to the zero vector), taken after the
+      block's merge (Sec. IV, exit-head description).
+  exit: head_b as above, c = max softmax
       = 1 / sum_k exp(l_k - l_max); exit iff delta < 1 and c >= delta
       (Eq. 6-7).  Exited samples return head_b's logits.
-  prune: score = head-mean CLS attention probability of block b (added up
-      through block b's merge); keep CLS + top floor(tau' N) patch tokens,
+  prune: score, rule "cls_attn" = head-mean CLS attention probability of
+      block b (added up through block b's merge); rule "learned" = the
+      linear scorer s_i = w . z_i + beta on the hidden states after the
+      merge (Eq. 8); keep CLS + top floor(tau' N) patch tokens,
       tau' = min(1, max(0, 1 - rho (1 - tau_b))), ties -> lower position,
       order kept; only samples that did not exit (Eq. 8, Sec. III-B).
 
 Decision margins (in O(1) units) are logged for every discrete decision:
 argmax best - second similarity, top-r gap s_(r) - s_(r+1), router: the
-change of m that moves 2 rho m r_b + 1/2 across an integer (unclamped
-only), exit |c - delta|, prune N (s_(k) - s_(k+1)).
+change of m that moves the count expression across an integer (unclamped
+only), exit |c - delta|, prune N (s_(k) - s_(k+1)) for CLS-attention scores
+(probabilities of order 1/N) and s_(k) - s_(k+1) for learned scores.
 
 Follow mode: given another implementation's decisions (``follow``), the
 oracle checks each against its own and adopts it only when the disagreement
@@ -138,7 +150,8 @@ def prepare_weights(W: dict, mode: str) -> dict:
     out = {}
     for k, v in W.items():
         leaf = k.split(".")[-1]
-        if leaf in ("pe_w", "qkv_w", "proj_w", "fc1_w", "fc2_w", "ew", "head_w"):
+        if leaf in ("pe_w", "qkv_w", "proj_w", "fc1_w", "fc2_w", "ew", "ew1",
+                    "ew2", "head_w"):
             out[k] = _rnd(v, mode)
         else:
             out[k] = np.asarray(v, dtype=F32)
@@ -216,6 +229,35 @@ def head_logits(x_cls, g, b, Wh, bh, mode):
     return (_mm(y, Wh.T) + bh)[0].astype(F32)
 
 
+def mlp_head_logits(v, g, b, W1, b1, W2, b2, mode):
+    """2-layer MLP head on a d-vector: LN, W1 + b1, exact GELU, W2 + b2."""
+    y = _rnd(layer_norm(v[None, :], g, b), mode)
+    h = _rnd(gelu(_mm(y, W1.T) + b1), mode)
+    return (_mm(h, W2.T) + b2)[0].astype(F32)
+
+
+def spatial_pool(x, s):
+    """Size-weighted mean of the patch rows: sum_t s_t x_t / sum_t s_t over
+    t >= 1, summed in token order; zero vector without patch rows."""
+    if x.shape[0] <= 1:
+        return np.zeros(x.shape[1], dtype=F32)
+    num = np.zeros(x.shape[1], dtype=F32)
+    den = F32(0.0)
+    for t in range(1, x.shape[0]):
+        num = num + s[t] * x[t]
+        den = den + s[t]
+    return (num / den).astype(F32)
+
+
+def exit_logits(x, s, Wb, kind, mode):
+    """head_b of Eq. 6 for the exit-head kind of the block."""
+    if kind == "linear":
+        return head_logits(x[0], Wb["eln_g"], Wb["eln_b"], Wb["ew"], Wb["eb"], mode)
+    v = x[0] if kind == "cls_mlp" else spatial_pool(x, s)
+    return mlp_head_logits(v, Wb["eln_g"], Wb["eln_b"], Wb["ew1"], Wb["eb1"],
+                           Wb["ew2"], Wb["eb2"], mode)
+
+
 def max_softmax(l):
     """c = max_k softmax(l)_k = 1 / sum_k exp(l_k - max l)  (Eq. 7)."""
     e = np.exp(l - l.max())
@@ -223,20 +265,27 @@ def max_softmax(l):
 
 
 # ------------------------------------------------------------ router ------
-def router(x_cls, w, beta, rho, r_b, N):
-    """m = sigmoid(w . z_cls + beta) (Eq. 4); r from the rho-scaled budget.
+def router(x_cls, w, beta, rho, r_b, N, rule="budget"):
+    """m = sigmoid(w . z_cls + beta) (Eq. 4); r by the merge-count rule.
 
+    "budget":   r = clamp(floor(2 rho m r_b + 1/2), 0, floor(N/2));
+    "fraction": r = min(floor(((rho m) N) / 2), floor(N/2)) (Sec. III-C
+                with the rescaled ratio of Eq. 5).
     Returns (m, r, margin).  The margin is in units of m, like every other
-    decision margin in O(1) units: the distance of 2 rho m r_b + 1/2 to the
-    nearest integer divided by 2 rho r_b, i.e. how far m must move to change
-    r; +inf when the count is clamped or does not depend on m.
+    decision margin in O(1) units: the distance of the count expression to
+    the nearest integer divided by its slope in m, i.e. how far m must move
+    to change r; +inf when the count is clamped or does not depend on m.
     """
     z = F32(np.dot(w, x_cls)) + F32(beta)
     m = F32(1.0) / (F32(1.0) + np.exp(-z, dtype=F32))
-    t = ((2.0 * float(rho)) * float(m)) * float(r_b) + 0.5
+    if rule == "fraction":
+        t = ((float(rho) * float(m)) * float(N)) * 0.5
+        slope = 0.5 * float(rho) * float(N)
+    else:
+        t = ((2.0 * float(rho)) * float(m)) * float(r_b) + 0.5
+        slope = 2.0 * float(rho) * float(r_b)
     r_raw = math.floor(t)
     r = min(max(r_raw, 0), N // 2)
-    slope = 2.0 * float(rho) * float(r_b)
     margin = abs(t - round(t)) / slope if (r == r_raw and slope > 0) else math.inf
     return m, int(r), margin
 
@@ -321,18 +370,26 @@ def apply_merge(x, s, score, origin, A, B, chosen, dst):
 
 
 # ------------------------------------------------------------- prune ------
-def prune_plan(score, k):
+def learned_scores(x, w, beta):
+    """s_i = h_b(z_i) = w . z_i + beta for every row (Eq. 8, linear h_b)."""
+    return (_mm(x, w) + F32(beta)).astype(F32)
+
+
+def prune_plan(score, k, unit=None):
     """Top-k patch tokens by score (ties -> lower position); CLS excluded.
 
-    Returns (kept patch positions in order, margin N (s_(k) - s_(k+1))).
+    Returns (kept patch positions in order, margin unit (s_(k) - s_(k+1)),
+    order); ``unit`` defaults to N (probability scores of order 1/N).
     """
     sc = score[1:]
     N = sc.shape[0]
+    if unit is None:
+        unit = float(N)
     order = np.argsort(-sc, kind="stable")
     kept = np.sort(order[:k])
     margin = math.inf
     if 0 < k < N:
-        margin = float(N) * float(sc[order[k - 1]] - sc[order[k]])
+        margin = float(unit) * float(sc[order[k - 1]] - sc[order[k]])
     return kept, margin, order
 
 
@@ -363,6 +420,10 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
     if delta is None:
         delta = cfg["delta"]
     delta_of = {b: F32(dl) for b, dl in zip(cfg["exits"], delta)}
+    kind_of = dict(zip(cfg["exits"], cfg.get("exit_kind",
+                                             ("linear",) * len(cfg["exits"]))))
+    merge_rule = cfg.get("merge_rule", "budget")
+    learned = cfg.get("prune_rule", "cls_attn") == "learned"
     x = patch_embed(img, W, cfg, mode)
     T0 = x.shape[0]
     s = np.ones(T0, dtype=F32)
@@ -374,14 +435,14 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
         counts[b - 1] = x.shape[0]
         Wb = _b_weights(W, b)
         isM, isE, isP = b in cfg["merges"], b in cfg["exits"], b in cfg["prunes"]
-        x, score = block(x, s, Wb, cfg, mode, want_cls=isP)
+        x, score = block(x, s, Wb, cfg, mode, want_cls=isP and not learned)
         fb = None if follow is None else follow.get(b)
         tb = dict(T=x.shape[0])
         # ---- merge (Alg. 1, merge branch; Sec. III-C)
         if isM:
             N = x.shape[0] - 1
             m, r, rmargin = router(x[0], Wb["router_w"], Wb["router_b"][0],
-                                   rho, cfg["r_b"][b - 1], N)
+                                   rho, cfg["r_b"][b - 1], N, merge_rule)
             tb.update(m=float(m), r=r, router_margin=rmargin)
             if fb is not None and fb["r"] != r:
                 if not (rmargin < tol and abs(fb["r"] - r) == 1):
@@ -407,7 +468,7 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
             tb["ids_after_merge"] = origin.copy()
         # ---- exit check (Alg. 1, exit branch; Sec. III-D)
         if isE:
-            lg = head_logits(x[0], Wb["eln_g"], Wb["eln_b"], Wb["ew"], Wb["eb"], mode)
+            lg = exit_logits(x, s, Wb, kind_of[b], mode)
             c = max_softmax(lg)
             dl = delta_of[b]
             fire = bool(dl < F32(1.0) and c >= dl)
@@ -427,11 +488,17 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
         if isP:
             N = x.shape[0] - 1
             k = keep_count(N, cfg["tau_b"][b - 1], rho)
-            kept, pmargin, order = prune_plan(score, k)
+            unit = None
+            if learned:
+                score = learned_scores(x, Wb["prune_w"], Wb["prune_b"][0])
+                unit = 1.0
+            kept, pmargin, order = prune_plan(score, k, unit)
             tb.update(k=k, prune_margin=pmargin)
+            if learned:
+                tb["scores"] = score.copy()
             if fb is not None:
                 kept = _follow_prune(b, score, k, kept, order, origin, fb["ids"],
-                                     tol, adopted)
+                                     tol, adopted, unit)
             rows = np.concatenate([[0], 1 + kept]).astype(np.int64)
             x, s, origin = x[rows], s[rows], origin[rows]
         tb["ids"] = origin.copy()
@@ -482,9 +549,11 @@ def _follow_merge(b, plan, r, origin, fmerge, tol, adopted):
     return chosen_f, dst_f
 
 
-def _follow_prune(b, score, k, kept, order, origin, fids, tol, adopted):
+def _follow_prune(b, score, k, kept, order, origin, fids, tol, adopted,
+                  unit=None):
     sc = score[1:]
     N = sc.shape[0]
+    U = float(N) if unit is None else float(unit)
     pos_of = {int(o): i for i, o in enumerate(origin[1:])}
     fids = [int(t) for t in fids]
     if len(fids) != k + 1 or fids[0] != int(origin[0]):
@@ -500,10 +569,10 @@ def _follow_prune(b, score, k, kept, order, origin, fids, tol, adopted):
     s_k = sc[order[k - 1]] if k > 0 else np.inf
     s_k1 = sc[order[k]] if k < N else -np.inf
     for t in theirs - own:
-        if not N * sc[t] >= N * s_k - tol:
+        if not U * sc[t] >= U * s_k - tol:
             raise DecisionMismatch(f"block {b}: kept pos {t} score {sc[t]} vs s_k {s_k}")
     for t in own - theirs:
-        if not N * sc[t] <= N * s_k1 + tol:
+        if not U * sc[t] <= U * s_k1 + tol:
             raise DecisionMismatch(f"block {b}: pruned pos {t} score {sc[t]} vs s_k+1 {s_k1}")
     adopted.append((b, "prune"))
     return np.array(sorted(theirs), dtype=np.int64)
@@ -537,10 +606,15 @@ def executed_flops(cfg, token_counts, exit_block):
     """Algorithmic FLOPs actually executed for one sample.
 
     Per executed block with T tokens: 24 T d^2 (+ 8 T d mlp/d correction
-    for mlp != 4d) + 4 T^2 d; patch embed 2 N0 (C p^2) d; 2 d C per head
-    evaluated (exit heads reached, final head if no exit).
+    for mlp != 4d) + 4 T^2 d; patch embed 2 N0 (C p^2) d; per head
+    evaluated (exit heads reached, final head if no exit) 2 d C for a
+    linear head and 2 d h + 2 h C for an MLP head of hidden width h.  Only
+    matrix products count (no LayerNorm, pooling, softmax or scorer).
     """
     d, mlp, C = cfg["d"], cfg["mlp"], cfg["C"]
+    kinds = dict(zip(cfg["exits"], cfg.get("exit_kind",
+                                           ("linear",) * len(cfg["exits"]))))
+    hx = cfg.get("exit_hidden", 0)
     f = 2 * cfg["N0"] * cfg["patch_dim"] * d
     for b in range(1, cfg["L"] + 1):
         T = int(token_counts[b - 1])
@@ -548,7 +622,7 @@ def executed_flops(cfg, token_counts, exit_block):
             continue
         f += 2 * T * d * 3 * d + 2 * T * d * d + 4 * T * d * mlp + 4 * T * T * d
         if b in cfg["exits"]:
-            f += 2 * d * C
+            f += 2 * d * C if kinds[b] == "linear" else 2 * d * hx + 2 * hx * C
     if exit_block == cfg["L"]:
         f += 2 * d * C
     return f

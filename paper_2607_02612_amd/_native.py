@@ -24,7 +24,9 @@ class FusionInfo(ctypes.Structure):
                 ("exit_mask", c_uint32), ("prune_mask", c_uint32),
                 ("n_exit", c_int32), ("exit_blocks", c_int32 * MAX_LAYERS),
                 ("r_b", c_int32 * MAX_LAYERS), ("tau_b", c_double * MAX_LAYERS),
-                ("delta", c_float * MAX_LAYERS), ("rho", c_double)]
+                ("delta", c_float * MAX_LAYERS), ("rho", c_double),
+                ("merge_rule", c_int32), ("prune_rule", c_int32),
+                ("exit_kind", c_int32 * MAX_LAYERS), ("exit_hidden", c_int32)]
 
     def as_dict(self) -> dict:
         out = {}
@@ -36,6 +38,7 @@ class FusionInfo(ctypes.Structure):
         out["delta"] = out["delta"][:out["n_exit"]]
         out["r_b"] = out["r_b"][:L]
         out["tau_b"] = out["tau_b"][:L]
+        out["exit_kind"] = out["exit_kind"][:L]
         return out
 
 

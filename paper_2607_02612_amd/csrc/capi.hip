@@ -35,8 +35,8 @@ int fail(int code, const std::string& msg) {
 
 // ----------------------------------------------------------- blob format --
 constexpr char kMagic[8] = {'F', 'U', 'S', 'N', 'V', 'I', 'T', '\0'};
-constexpr uint32_t kVersion = 1;
-constexpr size_t kHeaderBytes = 584;  // see the blob writer's layout
+constexpr uint32_t kVersion = 2;
+constexpr size_t kHeaderBytes = 724;  // see the blob writer's layout
 constexpr size_t kEntryBytes = 68;
 
 struct TensorRef {
@@ -52,6 +52,9 @@ struct Config {
   int r_b[FUSION_MAX_LAYERS];
   double tau_b[FUSION_MAX_LAYERS];
   float delta_b[FUSION_MAX_LAYERS];
+  int merge_rule, prune_rule;            // FUSION_MERGE_*, FUSION_PRUNE_*
+  int exit_kind[FUSION_MAX_LAYERS];      // FUSION_EXIT_* (exit blocks)
+  int exit_hidden;
   int n0, pdim, dh;
   std::vector<int> exits;
 };
@@ -91,8 +94,20 @@ std::vector<std::pair<std::string, std::vector<int64_t>>> expected_tensors(const
     if (c.exit_mask >> (b - 1) & 1) {
       v.push_back({p + "eln_g", {d}});
       v.push_back({p + "eln_b", {d}});
-      v.push_back({p + "ew", {C, d}});
-      v.push_back({p + "eb", {C}});
+      if (c.exit_kind[b - 1] == FUSION_EXIT_LINEAR) {
+        v.push_back({p + "ew", {C, d}});
+        v.push_back({p + "eb", {C}});
+      } else {
+        const int64_t hx = c.exit_hidden;
+        v.push_back({p + "ew1", {hx, d}});
+        v.push_back({p + "eb1", {hx}});
+        v.push_back({p + "ew2", {C, hx}});
+        v.push_back({p + "eb2", {C}});
+      }
+    }
+    if ((c.prune_mask >> (b - 1) & 1) && c.prune_rule == FUSION_PRUNE_LEARNED) {
+      v.push_back({p + "prune_w", {d}});
+      v.push_back({p + "prune_b", {1}});
     }
   }
   v.push_back({"norm_g", {d}});
@@ -138,6 +153,23 @@ int parse_blob(const void* blob, size_t bytes, Config& c,
       if (!(c.delta_b[b] >= 0.f && c.delta_b[b] <= 1.f)) return fail(FUSION_E_BLOB, "bad exit threshold");
     }
   }
+  c.merge_rule = (int)rd<uint32_t>(p, 580);
+  c.prune_rule = (int)rd<uint32_t>(p, 584);
+  if (c.merge_rule > FUSION_MERGE_FRACTION) return fail(FUSION_E_BLOB, "unknown merge rule");
+  if (c.prune_rule > FUSION_PRUNE_LEARNED) return fail(FUSION_E_BLOB, "unknown prune rule");
+  bool any_mlp = false;
+  for (int b = 0; b < FUSION_MAX_LAYERS; b++) {
+    const uint32_t k = rd<uint32_t>(p, 588 + 4 * b);
+    const bool is_exit = b < c.L && (c.exit_mask >> b & 1);
+    if (k > FUSION_EXIT_POOL_MLP || (k != 0 && !is_exit))
+      return fail(FUSION_E_BLOB, "bad exit-head kind");
+    c.exit_kind[b] = (int)k;
+    any_mlp = any_mlp || k != FUSION_EXIT_LINEAR;
+  }
+  const uint32_t hx = rd<uint32_t>(p, 716);
+  if (any_mlp && (hx == 0 || hx > 8192 || hx % (c.precision == 1 ? 64 : 32)))
+    return fail(FUSION_E_BLOB, "exit hidden width must be a multiple of 64 (bf16) or 32 (fp32), at most 8192");
+  c.exit_hidden = any_mlp ? (int)hx : 0;
   c.n0 = (c.img / c.patch) * (c.img / c.patch);
   c.pdim = c.in_ch * c.patch * c.patch;
   c.dh = c.d / c.heads;
@@ -151,7 +183,7 @@ int parse_blob(const void* blob, size_t bytes, Config& c,
   if (c.precision == 1 && (c.d % 64 || c.mlp % 64 || c.pdim % 64))
     return fail(FUSION_E_BLOB, "bf16 path needs width, MLP width and patch size multiples of 64");
 
-  const uint32_t nt = rd<uint32_t>(p, 580);
+  const uint32_t nt = rd<uint32_t>(p, 720);
   auto exp = expected_tensors(c);
   if (nt != exp.size()) return fail(FUSION_E_BLOB, "tensor count does not match the header");
   if (kHeaderBytes + (size_t)nt * kEntryBytes > bytes) return fail(FUSION_E_BLOB, "truncated tensor table");
@@ -196,8 +228,12 @@ void fill_info(const Config& c, fusion_info* o) {
   for (int b = 0; b < FUSION_MAX_LAYERS; b++) {
     o->r_b[b] = c.r_b[b];
     o->tau_b[b] = c.tau_b[b];
+    o->exit_kind[b] = c.exit_kind[b];
   }
   o->rho = 1.0;
+  o->merge_rule = c.merge_rule;
+  o->prune_rule = c.prune_rule;
+  o->exit_hidden = c.exit_hidden;
 }
 
 uint16_t host_bf16(float f) {
@@ -521,6 +557,11 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
   std::vector<TensorRef> tensors;
   if (int rc = parse_blob(blob, blob_bytes, c, tensors)) return rc;
 
+  for (int b = 0; b < c.L; b++)
+    if (c.exit_kind[b] != FUSION_EXIT_LINEAR)
+      return fail(FUSION_E_BLOB, "MLP exit heads are not implemented on the GPU yet");
+  if (c.prune_rule != FUSION_PRUNE_CLS_ATTN || c.merge_rule != FUSION_MERGE_BUDGET)
+    return fail(FUSION_E_BLOB, "this merge or prune rule is not implemented on the GPU yet");
   fusion_model* m = new fusion_model();
   m->cfg = c;
   m->max_batch = max_batch;

@@ -16,6 +16,29 @@ the fixed thresholds (0.5 / 0.6) inside the confidence distribution (about
 20-80 % early exits); DeiT-S (224 and 384) use 6.0, whose confidences spread
 over roughly 0.3-0.95 so that thresholds set at exit-rate percentiles are
 well separated.
+
+Rules (strings, read by both sides through the blob header):
+``merge_rule``  "budget"   -- r = clamp(floor(2 rho m r_b + 1/2), 0, N/2);
+                "fraction" -- r = floor(rho m N / 2), at most N/2: the merge
+                              ratio of Sec. III-C applied to the candidate
+                              pairs, rescaled by the profile ratio of Eq. 5.
+``prune_rule``  "cls_attn" -- token scores = head-mean CLS attention;
+                "learned"  -- s_i = w . z_i + beta, a linear scorer h_b
+                              (Eq. 8) with weights prune_w, prune_b.
+``exit_kind``   per exit block: "linear" (LN + linear on CLS), "cls_mlp"
+                (LN + 2-layer MLP on CLS) or "pool_mlp" (size-weighted mean
+                of the patch tokens, then LN + 2-layer MLP); ``exit_hidden``
+                is the MLP hidden width.
+
+The ``*_paper`` workloads instantiate Tab. I: M = {3,5,7}, E = {8,10} with
+a SpatialPool MLP head at block 8 and a CLS MLP head at block 10, P =
+{9,10} with the learned scorer, delta = (0.8, 0.95), tau = 0.7, merge
+ratios from the routers.  Hidden width 2d gives 2 x (d 2d + 2d C) ~ 2.1M
+head parameters at DeiT-S, the total the paper states.  The router bias
+-2 starts the merge ratio near sigmoid(-2) = 0.12 (about 11 of 98 pairs at
+block 3), and ``exit_gain`` 60 puts about 85-90 % of the block-8
+confidences above 0.8 with random backbones (the trained exit rate at
+block 8 is about 89 %, Tab. VII).
 """
 from __future__ import annotations
 
@@ -46,6 +69,23 @@ CONFIGS = {
     "deit_s_384": dict(_BASE_DEIT, index=5, img=384, d=384, H=6, mlp=1536,
                        batch=64, merges=tuple(range(1, 13)), r=24,
                        delta=0.6, exit_gain=6.0),
+    # Tab. I layer sets and rules at the tiny shape (fp32, parity workload).
+    "tiny_paper": dict(index=6, img=32, patch=4, in_ch=3, d=64, H=2, L=4,
+                       mlp=256, C=10, batch=16, precision="fp32",
+                       prop_attn=1, merges=(1, 2), r=0, exits=(2, 3),
+                       delta=(0.5, 0.6), prunes=(3, 4), tau=0.7,
+                       exit_gain=3.0, merge_rule="fraction",
+                       prune_rule="learned",
+                       exit_kind=("pool_mlp", "cls_mlp"), exit_hidden=128,
+                       router_bias=-1.0),
+    # Tab. I: DeiT-S with the paper's layer sets, heads and rules.
+    "deit_s_paper": dict(_BASE_DEIT, index=7, d=384, H=6, mlp=1536,
+                         batch=256, merges=(3, 5, 7), r=0, exits=(8, 10),
+                         delta=(0.8, 0.95), prunes=(9, 10), tau=0.7,
+                         exit_gain=60.0, merge_rule="fraction",
+                         prune_rule="learned",
+                         exit_kind=("pool_mlp", "cls_mlp"), exit_hidden=768,
+                         router_bias=-2.0),
 }
 
 
@@ -59,6 +99,15 @@ def get(name: str, **overrides) -> dict:
     cfg["N0"] = g * g
     cfg["dh"] = cfg["d"] // cfg["H"]
     cfg["patch_dim"] = cfg["in_ch"] * cfg["patch"] * cfg["patch"]
+    cfg.setdefault("merge_rule", "budget")
+    cfg.setdefault("prune_rule", "cls_attn")
+    cfg.setdefault("exit_hidden", 0)
+    cfg.setdefault("router_bias", 0.0)
+    if "exit_kind" not in cfg:
+        cfg["exit_kind"] = tuple("linear" for _ in cfg["exits"])
+    cfg["exit_kind"] = tuple(cfg["exit_kind"])
+    if len(cfg["exit_kind"]) != len(cfg["exits"]):
+        raise ValueError("one exit_kind per exit block")
     if isinstance(cfg.get("delta"), (int, float)):
         cfg["delta"] = tuple(float(cfg["delta"]) for _ in cfg["exits"])
     cfg["r_b"] = tuple(cfg["r"] if b in cfg["merges"] else 0

@@ -10,8 +10,12 @@ Init (random-init backbone, N(0, 0.02) for cls, pos and every matrix):
     parameter cannot cancel out.
 Exit heads and the final classifier use N(0, (g/sqrt(d))^2) with
 g = cfg["exit_gain"], so that max-softmax confidences spread over (0, 1)
-instead of sitting near 1/C.  Router weights use ``router_std`` (0.02 by
-default; a larger value spreads the per-sample merge counts).
+instead of sitting near 1/C; for MLP exit heads the first layer is
+N(0, 1/d) (unit-scale hidden pre-activations) and the second
+N(0, (g/sqrt(hidden))^2).  Router weights use ``router_std`` (0.02 by
+default; a larger value spreads the per-sample merge counts) and the bias
+``router_bias`` (the workload's value by default).  The learned pruning
+scorer uses N(0, 1/d), bias 0 (plain) or N(0, 0.05) (random).
 
 Tensor names, order and layouts are the ones the C library's blob parser
 expects (see ``synth.blob``):
@@ -20,7 +24,9 @@ expects (see ``synth.blob``):
   qkv_b[3d], proj_w[d, d], proj_b, ln2_g, ln2_b, fc1_w[mlp, d], fc1_b,
   fc2_w[d, mlp], fc2_b;
   per merge block: router_w[d], router_b[1];
-  per exit block: eln_g, eln_b, ew[C, d], eb[C];
+  per exit block: eln_g, eln_b, then ew[C, d], eb[C] ("linear") or
+      ew1[hidden, d], eb1[hidden], ew2[C, hidden], eb2[C] (MLP kinds);
+  per prune block with the learned scorer: prune_w[d], prune_b[1];
   final: norm_g, norm_b, head_w[C, d], head_b[C].
 """
 from __future__ import annotations
@@ -44,16 +50,26 @@ def tensor_specs(cfg: dict):
         if b in cfg["merges"]:
             specs += [(p + "router_w", (d,)), (p + "router_b", (1,))]
         if b in cfg["exits"]:
-            specs += [(p + "eln_g", (d,)), (p + "eln_b", (d,)),
-                      (p + "ew", (C, d)), (p + "eb", (C,))]
+            kind = cfg["exit_kind"][cfg["exits"].index(b)]
+            specs += [(p + "eln_g", (d,)), (p + "eln_b", (d,))]
+            if kind == "linear":
+                specs += [(p + "ew", (C, d)), (p + "eb", (C,))]
+            else:
+                hx = cfg["exit_hidden"]
+                specs += [(p + "ew1", (hx, d)), (p + "eb1", (hx,)),
+                          (p + "ew2", (C, hx)), (p + "eb2", (C,))]
+        if b in cfg["prunes"] and cfg["prune_rule"] == "learned":
+            specs += [(p + "prune_w", (d,)), (p + "prune_b", (1,))]
     specs += [("norm_g", (d,)), ("norm_b", (d,)),
               ("head_w", (C, d)), ("head_b", (C,))]
     return specs
 
 
 def make_weights(cfg: dict, seed: int | None = None, affine: str = "plain",
-                 router_std: float = 0.02, router_bias: float = 0.0) -> dict:
+                 router_std: float = 0.02, router_bias: float | None = None) -> dict:
     """Draw every tensor of ``tensor_specs(cfg)`` as float32."""
+    if router_bias is None:
+        router_bias = cfg.get("router_bias", 0.0)
     if seed is None:
         seed = cfg["index"]
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -68,7 +84,8 @@ def make_weights(cfg: dict, seed: int | None = None, affine: str = "plain",
             else:
                 a = np.ones(shape)
         elif leaf in ("ln1_b", "ln2_b", "eln_b", "norm_b", "pe_b", "qkv_b",
-                      "proj_b", "fc1_b", "fc2_b", "eb", "head_b"):
+                      "proj_b", "fc1_b", "fc2_b", "eb", "eb1", "eb2", "head_b",
+                      "prune_b"):
             if affine == "random":
                 a = rng.normal(0.0, 0.05, size=shape)
             else:
@@ -79,6 +96,10 @@ def make_weights(cfg: dict, seed: int | None = None, affine: str = "plain",
             a = rng.normal(0.0, router_std, size=shape)
         elif leaf in ("ew", "head_w"):
             a = rng.normal(0.0, head_std, size=shape)
+        elif leaf in ("ew1", "prune_w"):
+            a = rng.normal(0.0, 1.0 / np.sqrt(d), size=shape)
+        elif leaf == "ew2":
+            a = rng.normal(0.0, cfg["exit_gain"] / np.sqrt(shape[1]), size=shape)
         else:  # cls, pos, pe_w, qkv_w, proj_w, fc1_w, fc2_w
             a = rng.normal(0.0, 0.02, size=shape)
         out[name] = np.ascontiguousarray(a, dtype=np.float32)
@@ -99,9 +120,20 @@ def backbone_param_count(cfg: dict) -> int:
     n = 0
     for name, shape in tensor_specs(cfg):
         leaf = name.split(".")[-1]
-        if leaf.startswith("router") or leaf in ("eln_g", "eln_b", "ew", "eb"):
+        if leaf.startswith("router") or leaf.startswith("prune") or leaf in (
+                "eln_g", "eln_b", "ew", "eb", "ew1", "eb1", "ew2", "eb2"):
             continue
         n += int(np.prod(shape))
+    return n
+
+
+def exit_head_param_count(cfg: dict) -> int:
+    """Parameters of the exit heads (LayerNorm included)."""
+    n = 0
+    for name, shape in tensor_specs(cfg):
+        if name.split(".")[-1] in ("eln_g", "eln_b", "ew", "eb", "ew1", "eb1",
+                                   "ew2", "eb2"):
+            n += int(np.prod(shape))
     return n
 
 

@@ -12,7 +12,8 @@ are the floors any other bf16 implementation (the GPU path included) must
 be allowed; the parity tests use a multiple of them where it exceeds the
 literal bounds (2e-2 for logits, 1e-3 for exit margins).
 
-Usage:  python tests/golden/make_noise_floor.py
+Usage:  python tests/golden/make_noise_floor.py [workload ...]
+        (with names: recompute only those rows of the plan, keep the rest)
 """
 from __future__ import annotations
 
@@ -30,7 +31,8 @@ from oracle import fusion_oracle as fo  # noqa: E402
 from synth import configs, images, weights  # noqa: E402
 
 PLAN = [("deit_ti", 1.0, 64), ("deit_s", 1.0, 32), ("deit_b", 1.0, 12),
-        ("deit_s_384", 0.5, 6), ("deit_s_384", 1.0, 6), ("deit_s_384", 1.5, 6)]
+        ("deit_s_384", 0.5, 6), ("deit_s_384", 1.0, 6), ("deit_s_384", 1.5, 6),
+        ("deit_s_paper", 1.0, 32)]
 
 
 def floor(name, rho, n):
@@ -55,13 +57,22 @@ def floor(name, rho, n):
 
 
 def main():
+    only = set(sys.argv[1:])
+    path = os.path.join(HERE, "noise_floor.json")
+    old = {}
+    if only and os.path.exists(path):
+        with open(path) as f:
+            old = {(w["workload"], w["rho"]): w for w in json.load(f)["workloads"]}
     out = {"method": __doc__.split("Usage")[0].strip(), "workloads": []}
     for name, rho, n in PLAN:
+        if only and name not in only and (name, rho) in old:
+            out["workloads"].append(old[(name, rho)])
+            continue
         t0 = time.time()
         r = floor(name, rho, n)
         out["workloads"].append(r)
         print(r, f"{time.time() - t0:.0f}s", flush=True)
-    with open(os.path.join(HERE, "noise_floor.json"), "w") as f:
+    with open(path, "w") as f:
         json.dump(out, f, indent=1)
 
 

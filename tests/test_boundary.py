@@ -83,7 +83,7 @@ def test_corrupt_blobs_are_rejected(tiny_blob):
     _expect(E, bytes(bad))
     # tensor name out of order
     bad = bytearray(b)
-    nm = 584
+    nm = blob.HEADER_BYTES
     bad[nm:nm + 3] = b"xyz"
     assert "expected tensor" in _expect(E, bytes(bad))
 
@@ -113,3 +113,27 @@ def test_profile_kind_names():
     n = lib.fusion_profile_kinds()
     names = [lib.fusion_profile_kind_name(k).decode() for k in range(n)]
     assert "attention" in names and "adapt" in names and len(set(names)) == n
+
+
+def test_blob_inspect_reads_paper_rules():
+    cfg = configs.get("deit_s_paper")
+    b = blob.pack(cfg, weights.make_weights(cfg))
+    info = blob_inspect(b)
+    assert info["merge_rule"] == 1 and info["prune_rule"] == 1
+    assert info["exit_hidden"] == 768
+    assert info["exit_kind"][7] == 2 and info["exit_kind"][9] == 1
+    assert info["exit_blocks"] == [8, 10]
+    assert info["delta"] == pytest.approx([0.8, 0.95])
+    # an exit-head kind on a block that has no exit head
+    bad = bytearray(b)
+    bad[588:592] = struct.pack("<I", 1)
+    assert "exit-head kind" in _expect(-2, bytes(bad))
+    # hidden width that the bf16 GEMMs cannot tile
+    bad = bytearray(b)
+    bad[716:720] = struct.pack("<I", 700)
+    assert "hidden width" in _expect(-2, bytes(bad))
+    # unknown rules
+    for off in (580, 584):
+        bad = bytearray(b)
+        bad[off:off + 4] = struct.pack("<I", 5)
+        assert "rule" in _expect(-2, bytes(bad))
