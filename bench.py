@@ -6,9 +6,22 @@ already resident in HBM.  Default workload: DeiT-S shape, batch 256, bf16,
 224x224 images, router strength 1; the headline line is taken at the
 0 %-early-exit threshold, and the 50 % and 90 % settings (thresholds from
 the oracle calibration in tests/golden/exit_thresholds.json) are reported
-alongside.  Prints one JSON line.
+alongside.
+
+Also reported (same JSON line):
+  paper     the Tab. I instantiation (DeiT-S, M = {3,5,7}, E = {8,10} with
+            MLP heads, P = {9,10} with the learned scorer) under the
+            balanced and power_save profiles and with adaptation off (plain
+            DeiT-S on the same weights): images/s, exit rates, executed
+            GFLOP/image and the reduction against dense DeiT-S, energy per
+            image from the GPU's energy counter and 100 Hz power samples;
+  ablation  single-mechanism and composed layer sets on one set of weights
+            (Tab. VII): executed-FLOPs reduction and images/s;
+  batch_sweep  images/s and ms/step against batch size for the profiles.
+Prints one JSON line.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
+                       [--no-paper] [--headline-only]
 """
 from __future__ import annotations
 
@@ -27,18 +40,36 @@ BF16_PEAK = 2.5e15   # MI355X dense bf16 MFMA, FLOP/s
 HBM_PEAK = 8.0e12    # MI355X HBM3E, B/s
 
 
+def head_flops(cfg, b):
+    """Matrix FLOPs of exit head b: 2 d C (linear) or 2 d h + 2 h C (MLP)."""
+    d, C = cfg["d"], cfg["C"]
+    kind = cfg["exit_kind"][cfg["exits"].index(b)]
+    if kind == "linear":
+        return 2.0 * d * C
+    h = cfg["exit_hidden"]
+    return 2.0 * d * h + 2.0 * h * C
+
+
 def executed_flops(cfg, counts, exit_block):
     """Algorithmic FLOPs the batch executed (per sample: patch embedding,
-    24 T d^2 + 4 T^2 d per block run (mlp = 4d), the heads evaluated)."""
+    2 T d (3d + d + 2 mlp) + 4 T^2 d per block run, the heads evaluated)."""
     d, mlp, C, L = cfg["d"], cfg["mlp"], cfg["C"], cfg["L"]
     T = counts.astype(np.float64)
     per_block = 2 * T * d * 3 * d + 2 * T * d * d + 4 * T * d * mlp + 4 * T * T * d
     f = per_block.sum()
     f += counts.shape[0] * 2.0 * cfg["N0"] * cfg["patch_dim"] * d
     for b in cfg["exits"]:
-        f += 2.0 * d * C * (counts[:, b - 1] > 0).sum()
+        f += head_flops(cfg, b) * (counts[:, b - 1] > 0).sum()
     f += 2.0 * d * C * (exit_block == L).sum()
     return float(f)
+
+
+def dense_flops(cfg):
+    """FLOPs of the plain backbone on one image (no exit heads, no token
+    reduction): the baseline of the FLOPs-reduction figures."""
+    d, mlp, C, L, T = cfg["d"], cfg["mlp"], cfg["C"], cfg["L"], cfg["N0"] + 1
+    blk = 2 * T * d * 3 * d + 2 * T * d * d + 4 * T * d * mlp + 4 * T * T * d
+    return float(L * blk + 2 * cfg["N0"] * cfg["patch_dim"] * d + 2 * d * C)
 
 
 def kernel_work(cfg, counts):
@@ -109,6 +140,244 @@ def cpu_baseline(cfg, W, imgs, n):
                       f"({dt:.1f} s wall)"}
 
 
+class EnergyMeter:
+    """GPU energy over a region, two ways: the difference of the device's
+    energy accumulator, and power samples at 100 Hz (current socket power)
+    integrated with the trapezoid rule, the sampling protocol of NVML-based
+    measurements.  Reads only; the device is matched to torch's device 0 by
+    PCI bus id.  ``error`` says why a reading is missing."""
+
+    def __init__(self):
+        self.ok, self.error, self.h = False, None, None
+        try:
+            import amdsmi
+            import torch
+            self.smi = amdsmi
+            amdsmi.amdsmi_init()
+            prop = torch.cuda.get_device_properties(0)
+            want = (int(prop.pci_domain_id), int(prop.pci_bus_id), int(prop.pci_device_id))
+            for h in amdsmi.amdsmi_get_processor_handles():
+                bdf = amdsmi.amdsmi_get_gpu_device_bdf(h)      # dddd:bb:dd.f
+                dom, bus, rest = bdf.split(":")
+                dev = rest.split(".")[0]
+                if (int(dom, 16), int(bus, 16), int(dev, 16)) == want:
+                    self.h = h
+            if self.h is None:
+                self.error = f"no amd-smi device with PCI id {want}"
+            else:
+                self.ok = True
+        except Exception as e:  # measurement is optional
+            self.error = f"{type(e).__name__}: {e}"
+
+    def _acc(self):
+        e = self.smi.amdsmi_get_energy_count(self.h)
+        return e["energy_accumulator"] * e["counter_resolution"] * 1e-6  # J
+
+    def _power(self):
+        p = self.smi.amdsmi_get_power_info(self.h)
+        v = p.get("current_socket_power")
+        if not isinstance(v, (int, float)):
+            v = p.get("average_socket_power")
+        return float(v) if isinstance(v, (int, float)) else None
+
+    def measure(self, fn):
+        """Run fn() (which synchronises the GPU) and return the energy."""
+        import threading
+        if not self.ok:
+            return {"error": self.error}
+        samples, stop = [], threading.Event()
+
+        def sampler():
+            while not stop.is_set():
+                try:
+                    w = self._power()
+                except Exception:
+                    w = None
+                if w is not None:
+                    samples.append((time.perf_counter(), w))
+                stop.wait(0.01)
+
+        th = threading.Thread(target=sampler, daemon=True)
+        try:
+            a0 = self._acc()
+        except Exception as e:
+            a0, self.error = None, f"energy counter: {e}"
+        th.start()
+        t0 = time.perf_counter()
+        fn()
+        t1 = time.perf_counter()
+        stop.set()
+        th.join()
+        out = {"seconds": t1 - t0, "power_samples": len(samples)}
+        if a0 is not None:
+            out["joules_counter"] = self._acc() - a0
+        if len(samples) >= 2:
+            j = 0.0
+            for (ta, wa), (tb, wb) in zip(samples, samples[1:]):
+                j += 0.5 * (wa + wb) * (tb - ta)
+            out["joules_sampled"] = j * (t1 - t0) / (samples[-1][0] - samples[0][0])
+            out["mean_power_w"] = float(np.mean([w for _, w in samples]))
+        return out
+
+
+def run_timed(model, x, out, steps, warmup, delta=None, rho=None):
+    """Warm up, then time `steps` runs on the current stream with HIP events;
+    returns ms per step and the last run's outputs (host)."""
+    import torch
+    if delta is not None:
+        model.set_exit_thresholds(list(delta))
+    if rho is not None:
+        model.set_router_strength(rho)
+    for _ in range(warmup):
+        model.run(x, out=out)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(steps):
+        model.run(x, out=out)
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps, out[1].cpu().numpy(), out[2].cpu().numpy()
+
+
+def summarize(cfg, B, ms, eb, counts):
+    fl = executed_flops(cfg, counts, eb)
+    exits = {str(b): float((eb == b).mean()) for b in cfg["exits"]}
+    return {"images_per_s": B / (ms / 1e3), "ms_per_step": ms,
+            "exit_rate": exits, "executed_gflop_per_image": fl / B / 1e9,
+            "flops_reduction_vs_dense": 1.0 - fl / B / dense_flops(cfg),
+            "pct_bf16_peak_executed": 100.0 * fl / (ms / 1e3) / BF16_PEAK,
+            "mean_tokens_per_block": float(counts[counts > 0].mean())}
+
+
+def paper_section(args, energy):
+    """Tab. I instantiation under its profiles; plain DeiT-S (the backbone
+    alone, same weights) as the baseline; the adaptive model with every
+    mechanism inert (delta = 1, rho = 0) shows the cost of the machinery."""
+    import torch
+    from paper_2607_02612_amd import FusionModel
+    from synth import blob, configs, images, weights
+    cfg = configs.get("deit_s_paper")
+    cfg_plain = configs.get("deit_s_paper", merges=(), exits=(), prunes=(),
+                            exit_kind=(), delta=())
+    W = weights.make_weights(cfg)
+    imgs = images.make_images(cfg)
+    B = cfg["batch"]
+    models = {"adaptive": FusionModel(blob.pack(cfg, W), B),
+              "plain": FusionModel(blob.pack(cfg_plain, W), B)}
+    x = torch.from_numpy(imgs).cuda()
+    settings = {name: dict(configs.profile_settings(name), model="adaptive")
+                for name in configs.PROFILES}
+    settings["adaptive_inert"] = dict(delta=(1.0, 1.0), rho=0.0, model="adaptive")
+    settings["plain"] = dict(delta=None, rho=None, model="plain")
+    cfg_of = {"adaptive": cfg, "plain": cfg_plain}
+
+    def go(name, xb, steps, warmup):
+        st = settings[name]
+        mdl = models[st["model"]]
+        ob = mdl.alloc_outputs(xb.shape[0])
+        return run_timed(mdl, xb, ob, steps, warmup, st["delta"], st["rho"])
+
+    res = {}
+    for name, st in settings.items():
+        ms, eb, cnt = go(name, x, args.steps, args.warmup)
+        r = summarize(cfg_of[st["model"]], B, ms, eb, cnt)
+        r.update(delta=None if st["delta"] is None else list(st["delta"]), rho=st["rho"])
+        res[name] = r
+    for name in res:
+        res[name]["speedup_vs_plain"] = res["plain"]["ms_per_step"] / res[name]["ms_per_step"]
+    # energy: a region of about two seconds per setting
+    for name, st in settings.items():
+        mdl = models[st["model"]]
+        ob = mdl.alloc_outputs(B)
+        n = max(1, int(2000.0 / res[name]["ms_per_step"]))
+
+        def loop():
+            for _ in range(n):
+                mdl.run(x, out=ob)
+            torch.cuda.synchronize()
+        e = energy.measure(loop)
+        if "joules_counter" in e:
+            e["mj_per_image_counter"] = 1e3 * e["joules_counter"] / (n * B)
+        if "joules_sampled" in e:
+            e["mj_per_image_sampled"] = 1e3 * e["joules_sampled"] / (n * B)
+        e["images"] = n * B
+        e["images_per_s_in_region"] = n * B / e["seconds"] if "seconds" in e else None
+        res[name]["energy"] = e
+    # batch sweep (Fig. 6 protocol: throughput and latency against batch)
+    sweep = {}
+    for b in (1, 8, 32, 64, 128, 256):
+        xb = x[:b].contiguous()
+        row = {}
+        for name in settings:
+            ms, _, _ = go(name, xb, max(10, args.steps // 2), 3)
+            row[name] = {"images_per_s": b / (ms / 1e3), "ms_per_step": ms}
+        for name in row:
+            row[name]["speedup_vs_plain"] = row["plain"]["ms_per_step"] / row[name]["ms_per_step"]
+        sweep[str(b)] = row
+    for mdl in models.values():
+        mdl.close()
+    return {"workload": f"deit_s_paper batch {B}: merge (fraction rule) at "
+                        f"{list(cfg['merges'])}, exit heads {list(cfg['exits'])} "
+                        f"({', '.join(cfg['exit_kind'])}, hidden {cfg['exit_hidden']}), "
+                        f"learned prune keep {cfg['tau']} at {list(cfg['prunes'])}",
+            "dense_gflop_per_image": dense_flops(cfg) / 1e9,
+            "profiles": res, "batch_sweep": sweep}
+
+
+ABLATION = [
+    # name, layer-set overrides (Tab. VII rows), profile
+    ("plain", dict(merges=(), exits=(), prunes=()), "balanced"),
+    ("pruning only", dict(merges=(), exits=()), "balanced"),
+    ("merging only", dict(exits=(), prunes=()), "balanced"),
+    ("early exit only", dict(merges=(), prunes=()), "balanced"),
+    ("parallel prune + exit", dict(merges=(), prunes=(3, 6, 9)), "balanced"),
+    ("sequential exit -> prune", dict(merges=()), "balanced"),
+    ("full sequential, fixed r=8 merges", dict(merge_rule="budget", r=8), "balanced"),
+    ("full sequential, merge routers", dict(), "balanced"),
+    ("full sequential, routers + power_save scaling", dict(), "power_save"),
+]
+
+
+def ablation_section(args):
+    """Tab. VII layer-set variants on one set of weights (a superset draw:
+    every tensor any variant reads)."""
+    import torch
+    from paper_2607_02612_amd import FusionModel
+    from synth import blob, configs, images, weights
+    sup = configs.get("deit_s_paper", prunes=(3, 6, 9, 10))
+    W = weights.make_weights(sup)
+    imgs = images.make_images(sup)
+    B = sup["batch"]
+    x = torch.from_numpy(imgs).cuda()
+    rows = {}
+    for name, over, prof in ABLATION:
+        o = dict(over)
+        if "exits" in o and not o["exits"]:
+            o.update(exit_kind=(), delta=())
+        cfg = configs.get("deit_s_paper", **o)
+        if cfg["merge_rule"] == "budget":
+            Wc = weights.zero_routers(cfg, W)       # m = 1/2: r = r_b
+        else:
+            Wc = W
+        st = configs.profile_settings(prof)
+        delta = st["delta"][:len(cfg["exits"])]
+        model = FusionModel(blob.pack(cfg, Wc), B)
+        out = model.alloc_outputs(B)
+        ms, eb, cnt = run_timed(model, x, out, args.steps, args.warmup,
+                                delta if cfg["exits"] else None, st["rho"])
+        r = summarize(cfg, B, ms, eb, cnt)
+        r.update(merges=list(cfg["merges"]), exits=list(cfg["exits"]),
+                 prunes=list(cfg["prunes"]), merge_rule=cfg["merge_rule"],
+                 delta=list(delta), rho=st["rho"])
+        rows[name] = r
+        model.close()
+    base = rows["plain"]["ms_per_step"]
+    for r in rows.values():
+        r["speedup_vs_plain"] = base / r["ms_per_step"]
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -119,6 +388,8 @@ def main():
     ap.add_argument("--cpu-images", type=int, default=48)
     ap.add_argument("--headline-only", action="store_true",
                     help="time only the 0 %% early-exit setting (for profiler runs)")
+    ap.add_argument("--no-paper", action="store_true",
+                    help="skip the Tab. I / Tab. VII / batch-sweep sections")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 256 MiB device-to-device copy, whose HBM "
                          "counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -239,6 +510,11 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
     }
+    if not (args.no_paper or args.headline_only):
+        model.close()
+        energy = EnergyMeter()
+        line["paper"] = paper_section(args, energy)
+        line["ablation"] = ablation_section(args)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(cfg, W, imgs, args.cpu_images)
     print(json.dumps(line), flush=True)

@@ -408,15 +408,16 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
             dst_origin}, "exit": bool, "ids": [origin ids after the block's
             adaptation]}} from another implementation (see module doc).
     tol:    decision margin under which a followed choice may differ; a
-            float, or {"exit": t_exit, "other": t} to give the exit rule its
-            own margin (in units of c).
+            float, or {"exit": t_exit, "other": t[, "prune": t_prune]} to
+            give the exit rule (units of c) and the prune rule (score
+            units) their own margins.
     Returns dict(logits, exit_block, token_counts[L], trace, adopted).
     """
     L = cfg["L"]
     if isinstance(tol, dict):
-        tol_exit, tol = tol["exit"], tol["other"]
+        tol_exit, tol_prune, tol = tol["exit"], tol.get("prune", tol["other"]), tol["other"]
     else:
-        tol_exit = tol
+        tol_exit = tol_prune = tol
     if delta is None:
         delta = cfg["delta"]
     delta_of = {b: F32(dl) for b, dl in zip(cfg["exits"], delta)}
@@ -498,7 +499,7 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
                 tb["scores"] = score.copy()
             if fb is not None:
                 kept = _follow_prune(b, score, k, kept, order, origin, fb["ids"],
-                                     tol, adopted, unit)
+                                     tol_prune, adopted, unit)
             rows = np.concatenate([[0], 1 + kept]).astype(np.int64)
             x, s, origin = x[rows], s[rows], origin[rows]
         tb["ids"] = origin.copy()

@@ -33,11 +33,14 @@ template <int TMAX_> struct AdSize {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ int merge_count(float m, double rho, int r_b, int N) {
-  // r = clamp(floor(((2 rho) m) r_b + 1/2), 0, floor(N/2)), every step an
-  // individually rounded IEEE double operation.
-  const double t = __dadd_rn(__dmul_rn(__dmul_rn(__dmul_rn(2.0, rho), (double)m),
-                                       (double)r_b), 0.5);
+__device__ __forceinline__ int merge_count(float m, double rho, int r_b, int N, int rule) {
+  // budget:   r = clamp(floor(((2 rho) m) r_b + 1/2), 0, floor(N/2));
+  // fraction: r = min(floor(((rho m) N) / 2), floor(N/2)) (Sec. III-C with
+  //           the rescaled ratio of Eq. 5);
+  // every step an individually rounded IEEE double operation.
+  const double t =
+      rule == 1 ? __dmul_rn(__dmul_rn(__dmul_rn(rho, (double)m), (double)N), 0.5)
+                : __dadd_rn(__dmul_rn(__dmul_rn(__dmul_rn(2.0, rho), (double)m), (double)r_b), 0.5);
   int r = (int)floor(t);
   if (r < 0) r = 0;
   if (r > N / 2) r = N / 2;
@@ -278,11 +281,14 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   __shared__ float red[16];
   __shared__ int ired[16];
 
+  // CLS-attention scores are gathered here and follow the merge; learned
+  // scores are computed after the merge from the merged hidden states
+  const bool attnP = a.isP && a.prune_rule == 0;
   for (int t = tid; t < T; t += AD_NT) {
     keepf[t] = 1;
     szs[t] = a.size[base + t];
   }
-  if (a.isP) {
+  if (attnP) {
     for (int t = tid; t < T; t += AD_NT) {
       float s = a.cls_scores[((size_t)i * a.H) * a.tmax + t];
       for (int h = 1; h < a.H; h++) s = s + a.cls_scores[((size_t)i * a.H + h) * a.tmax + t];
@@ -298,7 +304,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     for (int k = tid; k < d; k += AD_NT) z = fmaf(a.router_w[k], a.x[(size_t)base * d + k], z);
     z = bsum(z, red) + a.router_b[0];
     const float m = 1.0f / (1.0f + expf(-z));
-    r = merge_count(m, a.rho, a.r_b, N);
+    r = merge_count(m, a.rho, a.r_b, N, a.merge_rule);
     if (tid == 0) {
       if (a.tr_r) a.tr_r[tr_row] = r;
       if (a.tr_m) a.tr_m[tr_row] = m;
@@ -359,11 +365,11 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     for (int k = tid; k < ng; k += AD_NT) {
       const int q0 = glead[k], bb = cdst[q0];
       float den = szs[2 + 2 * bb];
-      float s2 = a.isP ? sc[2 + 2 * bb] : 0.f;
+      float s2 = attnP ? sc[2 + 2 * bb] : 0.f;
       for (int q = q0; q < r; q++) {
         if (cdst[q] != bb) continue;
         den = den + szs[1 + 2 * clist[q]];
-        if (a.isP) s2 = s2 + sc[1 + 2 * clist[q]];
+        if (attnP) s2 = s2 + sc[1 + 2 * clist[q]];
       }
       tmpf[k] = den;
       tmps[k] = s2;
@@ -372,7 +378,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     for (int k = tid; k < ng; k += AD_NT) {
       const int bb = cdst[glead[k]];
       a.size[base + 2 + 2 * bb] = tmpf[k];
-      if (a.isP) sc[2 + 2 * bb] = tmps[k];
+      if (attnP) sc[2 + 2 * bb] = tmps[k];
     }
     for (int q = tid; q < r; q += AD_NT) {
       const int aa = clist[q];
@@ -404,6 +410,29 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   }
 
   // ----------------------------------------------------------- prune --
+  if (a.isP && !fire && a.prune_rule == 1) {
+    // s_t = w . z_t + beta on the merged rows (Eq. 8): one half wave per
+    // token, 16-byte pieces, fixed-order half-wave sum.  The merge's row
+    // writes above are visible here: same workgroup, past a barrier.
+    const int hw = tid >> 5, hl = tid & 31, d4 = d >> 2;
+    const float4* w4 = (const float4*)a.prune_w;
+    const float pb = a.prune_b[0];
+    for (int t = 1 + hw; t < T; t += AD_NT / 32) {
+      if (!keepf[t]) continue;
+      const float4* xr = (const float4*)(a.x + (size_t)(base + t) * d);
+      float s = 0.f;
+      for (int q = hl; q < d4; q += 32) {
+        const float4 v = xr[q], w = w4[q];
+        s = fmaf(v.x, w.x, s);
+        s = fmaf(v.y, w.y, s);
+        s = fmaf(v.z, w.z, s);
+        s = fmaf(v.w, w.w, s);
+      }
+      s = half_sum(s);
+      if (hl == 0) sc[t] = s + pb;
+    }
+    __syncthreads();
+  }
   if (a.isP && !fire) {
     int ns = 0;
     for (int t = 1 + tid; t < T; t += AD_NT) ns += keepf[t];

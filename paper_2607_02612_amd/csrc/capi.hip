@@ -259,6 +259,9 @@ struct BlockW {
   const void *qkv_w, *proj_w, *fc1_w, *fc2_w;
   const float *router_w, *router_b, *eln_g, *eln_b, *eb;
   const void* ew;
+  // MLP exit heads (FUSION_EXIT_CLS_MLP / POOL_MLP) and the learned scorer
+  const float *eb1, *eb2, *prune_w, *prune_b;
+  const void *ew1, *ew2;
 };
 
 struct fusion_model {
@@ -283,6 +286,7 @@ struct fusion_model {
   void* qkv;   // [Mmax, 3d]
   void* ffn;   // [Mmax, mlp] (also the patch matrix)
   void* hc;    // [max_batch, d]
+  void* hbuf;  // [max_batch, exit_hidden] (MLP exit heads)
   float* head_buf;
   float* cls_scores;
   int* keep;
@@ -416,7 +420,8 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
       a.qkv = m->qkv; a.size = m->size[cur]; a.cu = m->cu[cur]; a.live = m->live[cur];
       a.cnt = m->cnt[cur]; a.H = c.heads; a.dh = c.dh; a.d = d; a.scale = scale;
       a.prop_attn = c.prop_attn; a.out = m->act;
-      a.cls_scores = isP ? m->cls_scores : nullptr; a.tmax = T0;
+      a.cls_scores = isP && c.prune_rule == FUSION_PRUNE_CLS_ATTN ? m->cls_scores : nullptr;
+      a.tmax = T0;
       a.token_counts = token_counts; a.L = L; a.b0 = b - 1;
       a.nlive_ub = B; a.T_ub = T_ub;
       HIP_OR_FAIL(launch_attention<T>(a, s));
@@ -445,12 +450,28 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
     }
     if (o.stop_block == b && o.stop_stage == 2) break;
     if (isE) {
+      // head_b of Eq. 6 on the state before this block's merge: the CLS row
+      // is untouched by merging and the size-weighted pool is invariant
+      // under it, so the logits equal those after the merge
       Prof p(m, s, K_EXIT_HEAD);
-      HIP_OR_FAIL(launch_layernorm<T>(m->x[cur], w.eln_g, w.eln_b, (T*)m->hc, d, m->cnt[cur],
-                                      m->cu[cur], m->live[cur], 1, B, nullptr, L, s));
-      Epi e{EPI_F32, m->head_buf, c.C, w.eb, nullptr, nullptr, 0};
-      HIP_OR_FAIL(launch_gemm<T>((const T*)m->hc, d, (const T*)w.ew, c.C, d, &m->cnt[cur]->nlive,
-                                 0, B, e, s));
+      const int kind = c.exit_kind[b - 1];
+      const int* nl = &m->cnt[cur]->nlive;
+      if (kind == FUSION_EXIT_POOL_MLP)
+        HIP_OR_FAIL(launch_pool_ln<T>(m->x[cur], m->size[cur], m->cu[cur], m->cnt[cur], w.eln_g,
+                                      w.eln_b, (T*)m->hc, d, B, s));
+      else
+        HIP_OR_FAIL(launch_layernorm<T>(m->x[cur], w.eln_g, w.eln_b, (T*)m->hc, d, m->cnt[cur],
+                                        m->cu[cur], m->live[cur], 1, B, nullptr, L, s));
+      if (kind == FUSION_EXIT_LINEAR) {
+        Epi e{EPI_F32, m->head_buf, c.C, w.eb, nullptr, nullptr, 0};
+        HIP_OR_FAIL(launch_gemm<T>((const T*)m->hc, d, (const T*)w.ew, c.C, d, nl, 0, B, e, s));
+      } else {
+        const int hx = c.exit_hidden;
+        Epi e1{EPI_GELU, m->hbuf, hx, w.eb1, nullptr, nullptr, 0};
+        HIP_OR_FAIL(launch_gemm<T>((const T*)m->hc, d, (const T*)w.ew1, hx, d, nl, 0, B, e1, s));
+        Epi e2{EPI_F32, m->head_buf, c.C, w.eb2, nullptr, nullptr, 0};
+        HIP_OR_FAIL(launch_gemm<T>((const T*)m->hbuf, hx, (const T*)w.ew2, c.C, hx, nl, 0, B, e2, s));
+      }
     }
     if (isM || isE || isP) {
       int exit_idx = 0;
@@ -464,6 +485,8 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
         a.live = m->live[cur]; a.cnt = m->cnt[cur];
         a.d = d; a.H = c.heads; a.n0 = n0; a.C = c.C; a.L = L; a.B = B; a.b = b;
         a.isM = isM; a.isE = isE; a.isP = isP;
+        a.merge_rule = c.merge_rule; a.prune_rule = c.prune_rule;
+        a.prune_w = w.prune_w; a.prune_b = w.prune_b;
         a.router_w = w.router_w; a.router_b = w.router_b; a.r_b = c.r_b[b - 1]; a.rho = m->rho;
         a.head_buf = m->head_buf; a.delta = isE ? m->delta[exit_idx] : 1.0f;
         a.logits = logits; a.exit_block = exit_block;
@@ -557,11 +580,6 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
   std::vector<TensorRef> tensors;
   if (int rc = parse_blob(blob, blob_bytes, c, tensors)) return rc;
 
-  for (int b = 0; b < c.L; b++)
-    if (c.exit_kind[b] != FUSION_EXIT_LINEAR)
-      return fail(FUSION_E_BLOB, "MLP exit heads are not implemented on the GPU yet");
-  if (c.prune_rule != FUSION_PRUNE_CLS_ATTN || c.merge_rule != FUSION_MERGE_BUDGET)
-    return fail(FUSION_E_BLOB, "this merge or prune rule is not implemented on the GPU yet");
   fusion_model* m = new fusion_model();
   m->cfg = c;
   m->max_batch = max_batch;
@@ -593,7 +611,8 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
   auto is_matrix = [](const std::string& n) {
     const std::string leaf = n.substr(n.find('.') == std::string::npos ? 0 : n.find('.') + 1);
     return leaf == "pe_w" || leaf == "qkv_w" || leaf == "proj_w" || leaf == "fc1_w" ||
-           leaf == "fc2_w" || leaf == "ew" || leaf == "head_w";
+           leaf == "fc2_w" || leaf == "ew" || leaf == "ew1" || leaf == "ew2" ||
+           leaf == "head_w";
   };
   std::vector<size_t> boff(tensors.size(), 0);
   if (c.precision == 1) {
@@ -640,6 +659,8 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
     w.fc2_w = Wm(p + "fc2_w");
     w.router_w = F(p + "router_w"); w.router_b = F(p + "router_b");
     w.eln_g = F(p + "eln_g"); w.eln_b = F(p + "eln_b"); w.eb = F(p + "eb"); w.ew = Wm(p + "ew");
+    w.eb1 = F(p + "eb1"); w.eb2 = F(p + "eb2"); w.ew1 = Wm(p + "ew1"); w.ew2 = Wm(p + "ew2");
+    w.prune_w = F(p + "prune_w"); w.prune_b = F(p + "prune_b");
   }
   // ---- workspace
   const size_t esz = c.precision == 1 ? 2 : 4;
@@ -658,6 +679,7 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
   m->qkv = dev_alloc<char>(m, Mmax * 3 * c.d * esz, &rc);
   m->ffn = dev_alloc<char>(m, Mmax * ffn_cols * esz, &rc);
   m->hc = dev_alloc<char>(m, (size_t)max_batch * c.d * esz, &rc);
+  m->hbuf = dev_alloc<char>(m, (size_t)max_batch * std::max(c.exit_hidden, 1) * esz, &rc);
   m->head_buf = (float*)dev_alloc<float>(m, (size_t)max_batch * c.C * 4, &rc);
   m->cls_scores = (float*)dev_alloc<float>(m, (size_t)max_batch * c.heads * (c.n0 + 1) * 4, &rc);
   m->keep = (int*)dev_alloc<int>(m, Mmax * 4, &rc);

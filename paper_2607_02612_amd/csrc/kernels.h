@@ -53,6 +53,13 @@ hipError_t launch_layernorm(const float* x, const float* g, const float* b,
                             const int* cu, const int* live, int cls_only,
                             int rows_ub, int* exit_block, int L, hipStream_t s);
 
+// LayerNorm of the size-weighted mean of each live sample's patch rows
+// (pooled exit heads): out[i] = LN(sum_t s_t x_t / sum_t s_t).
+template <typename T>
+hipError_t launch_pool_ln(const float* x, const float* size, const int* cu,
+                          const LiveCounts* cnt, const float* g, const float* b,
+                          T* out, int d, int nlive_ub, hipStream_t s);
+
 struct AttnArgs {
   const void* qkv;  // T [M, 3d]
   const float* size;
@@ -82,6 +89,10 @@ struct AdaptArgs {
   int d, H, n0, C, L, B;
   int b;  // 1-based block
   int isM, isE, isP;
+  int merge_rule;  // 0: budget, 1: fraction of the candidate pairs
+  int prune_rule;  // 0: CLS-attention scores, 1: learned scorer
+  const float* prune_w;  // [d] (learned scorer)
+  const float* prune_b;  // [1]
   const float* router_w;
   const float* router_b;
   int r_b;

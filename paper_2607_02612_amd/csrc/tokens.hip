@@ -122,6 +122,81 @@ template hipError_t launch_layernorm<bf16_t>(const float*, const float*, const f
                                              int, const LiveCounts*, const int*, const int*, int,
                                              int, int*, int, hipStream_t);
 
+// SpatialPool input of a pooled exit head: per live sample i,
+//   p = sum_t s_t x_t / sum_t s_t over its patch rows t = 1 .. T-1
+// (zero vector when T = 1), then out[i] = LN(p) with (g, b) in the storage
+// type of the precision path.  One 256-thread workgroup per sample: wave w
+// sums rows 1 + w, 5 + w, ... (lane l holds the 16-byte pieces l, l + 64,
+// l + 128), the four partial sums are added in wave order, and half wave 0
+// normalises the pooled row.  The pool reads the state before the block's
+// merge: size-weighted merging keeps sum_t s_t x_t and sum_t s_t, so the
+// pooled vector is the same before and after it.
+constexpr int POOL_MAXV = 3;  // 16-byte pieces per lane (d <= 768)
+template <typename T>
+__global__ __launch_bounds__(256) void pool_ln_kernel(
+    const float* __restrict__ x, const float* __restrict__ size,
+    const int* __restrict__ cu, const LiveCounts* cnt,
+    const float* __restrict__ g, const float* __restrict__ bb,
+    T* __restrict__ out, int d) {
+  const int i = blockIdx.x;
+  if (i >= cnt->nlive) return;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int base = cu[i], Tn = cu[i + 1] - base, n4 = d >> 2;
+  __shared__ __attribute__((aligned(16))) float part[4][4 * 64 * POOL_MAXV];
+  __shared__ float pden[4];
+  __shared__ __attribute__((aligned(16))) float pooled[4 * 64 * POOL_MAXV];
+  float4 acc[POOL_MAXV];
+#pragma unroll
+  for (int k = 0; k < POOL_MAXV; k++) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  float den = 0.f;
+  for (int t = 1 + wave; t < Tn; t += 4) {
+    const float st = size[base + t];
+    const float4* xr = (const float4*)(x + (size_t)(base + t) * d);
+#pragma unroll
+    for (int k = 0; k < POOL_MAXV; k++) {
+      const int q = lane + 64 * k;
+      if (q < n4) {
+        const float4 v = xr[q];
+        acc[k].x = fmaf(st, v.x, acc[k].x);
+        acc[k].y = fmaf(st, v.y, acc[k].y);
+        acc[k].z = fmaf(st, v.z, acc[k].z);
+        acc[k].w = fmaf(st, v.w, acc[k].w);
+      }
+    }
+    den += st;
+  }
+#pragma unroll
+  for (int k = 0; k < POOL_MAXV; k++) {
+    const int q = lane + 64 * k;
+    if (q < n4) *(float4*)&part[wave][4 * q] = acc[k];
+  }
+  if (lane == 0) pden[wave] = den;
+  __syncthreads();
+  const float D = ((pden[0] + pden[1]) + pden[2]) + pden[3];
+  for (int f = tid; f < d; f += 256) {
+    const float num = ((part[0][f] + part[1][f]) + part[2][f]) + part[3][f];
+    pooled[f] = D > 0.f ? num / D : 0.f;
+  }
+  __syncthreads();
+  if (tid < 32) ln_row_half<T>(pooled, d, tid, g, bb, out + (size_t)i * d, nullptr);
+}
+
+template <typename T>
+hipError_t launch_pool_ln(const float* x, const float* size, const int* cu,
+                          const LiveCounts* cnt, const float* g, const float* b,
+                          T* out, int d, int nlive_ub, hipStream_t s) {
+  if (nlive_ub <= 0) return hipSuccess;
+  if (d % 4 != 0 || d > 4 * 64 * POOL_MAXV) return hipErrorInvalidValue;
+  pool_ln_kernel<T><<<nlive_ub, 256, 0, s>>>(x, size, cu, cnt, g, b, out, d);
+  return hipGetLastError();
+}
+template hipError_t launch_pool_ln<float>(const float*, const float*, const int*,
+                                          const LiveCounts*, const float*, const float*,
+                                          float*, int, int, hipStream_t);
+template hipError_t launch_pool_ln<bf16_t>(const float*, const float*, const int*,
+                                           const LiveCounts*, const float*, const float*,
+                                           bf16_t*, int, int, hipStream_t);
+
 __global__ void copy_state_kernel(const float* __restrict__ x, const int* cu,
                                   const int* live, const LiveCounts* cnt,
                                   float* __restrict__ x_out, int* cu_out,

@@ -89,6 +89,25 @@ CONFIGS = {
 }
 
 
+# Operating profiles of the paper workloads (Sec. IV, Profiles; Tab. I):
+# per profile the exit thresholds delta_b and the target keep ratio tau_tgt;
+# the router strength is rho = (1 - tau_tgt) / (1 - tau_tgt(balanced)), the
+# rescaling of Eq. 5, which also scales the prune keep ratios.  balanced is
+# the reference profile of Tab. I.  The paper gives no power_save values;
+# this one takes tau_tgt = 0.5 and thresholds lowered by 0.1 / 0.05.
+PROFILES = {
+    "balanced": dict(delta=(0.8, 0.95), tau_tgt=0.7),
+    "power_save": dict(delta=(0.7, 0.9), tau_tgt=0.5),
+}
+
+
+def profile_settings(name: str, ref: str = "balanced") -> dict:
+    """delta and rho of a named profile (Eq. 5 ratio against ``ref``)."""
+    p, r = PROFILES[name], PROFILES[ref]
+    return dict(delta=tuple(p["delta"]),
+                rho=(1.0 - p["tau_tgt"]) / (1.0 - r["tau_tgt"]))
+
+
 def get(name: str, **overrides) -> dict:
     """Return a deep copy of workload ``name`` with derived sizes filled in."""
     cfg = copy.deepcopy(CONFIGS[name])

@@ -7,7 +7,8 @@ bf16emu mode: once with float32 (BLAS) accumulation of the matrix products
 and once accumulating in float64 (rounded once to float32).  The second run
 follows the first one's discrete decisions (any disagreement is adopted), so
 both share one trajectory; the only difference is summation order.  The
-maximum |logit difference| and |exit confidence difference| over the sample
+maximum |logit difference|, |exit confidence difference| and (learned
+prune scorer) |token score difference| over the sample
 are the floors any other bf16 implementation (the GPU path included) must
 be allowed; the parity tests use a multiple of them where it exceeds the
 literal bounds (2e-2 for logits, 1e-3 for exit margins).
@@ -40,7 +41,7 @@ def floor(name, rho, n):
     W = fo.prepare_weights(weights.make_weights(cfg), "bf16emu")
     imgs = images.make_images(cfg, batch=n)
     delta = [1.0] * len(cfg["exits"])
-    dl, dc = [], []
+    dl, dc, ds = [], [], []
     for i in range(n):
         a = fo.run_sample(imgs[i], W, cfg, "bf16emu", delta=delta, rho=rho)
         f = {b: dict(r=tb.get("r", 0), merge=tb.get("merge", {}), exit=False,
@@ -51,9 +52,16 @@ def floor(name, rho, n):
         dl.append(float(np.abs(a["logits"] - b_["logits"]).max()))
         dc.append(max(abs(a["trace"][e]["c"] - b_["trace"][e]["c"])
                       for e in cfg["exits"]))
-    return dict(workload=name, rho=rho, samples=n, max_dlogit=max(dl),
-                median_dlogit=float(np.median(dl)), max_dc=max(dc),
-                median_dc=float(np.median(dc)))
+        for p in cfg["prunes"]:
+            if "scores" in a["trace"].get(p, {}):
+                ds.append(float(np.abs(a["trace"][p]["scores"]
+                                       - b_["trace"][p]["scores"]).max()))
+    out = dict(workload=name, rho=rho, samples=n, max_dlogit=max(dl),
+               median_dlogit=float(np.median(dl)), max_dc=max(dc),
+               median_dc=float(np.median(dc)))
+    if ds:
+        out["max_dscore"] = max(ds)
+    return out
 
 
 def main():

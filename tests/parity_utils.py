@@ -56,6 +56,14 @@ def exit_tol(cfg, rho=1.0):
     return max(1e-3, FLOOR_FACTOR * noise_floor(cfg["name"], rho)["max_dc"])
 
 
+def prune_tol(cfg, rho=1.0):
+    """Prune-rule margin for learned scores (score units): 1e-3, raised to
+    2.5x the measured noise floor of the token scores on the bf16 path."""
+    if cfg["precision"] == "fp32" or cfg.get("prune_rule") != "learned":
+        return fo.TOL
+    return max(fo.TOL, FLOOR_FACTOR * noise_floor(cfg["name"], rho).get("max_dscore", 0.0))
+
+
 def exit_thresholds(name, rho):
     with open(os.path.join(GOLDEN, "exit_thresholds.json")) as f:
         data = json.load(f)
@@ -102,9 +110,14 @@ def gpu_run(model, imgs_dev, delta=None, rho=1.0, traced=True):
     return out
 
 
-def follow_of(cfg, res, i):
-    """The GPU's decisions for sample i in the oracle's follow format."""
+def follow_of(cfg, res, i, delta=None):
+    """The GPU's decisions for sample i in the oracle's follow format.  An
+    exit head at the last block fired iff its traced confidence reached the
+    threshold (exit_block = L either way)."""
     tr = res["trace"]
+    L = cfg["L"]
+    if delta is None:
+        delta = cfg["delta"]
     f = {}
     for b in range(1, cfg["L"] + 1):
         if res["counts"][i][b - 1] == 0:
@@ -117,7 +130,9 @@ def follow_of(cfg, res, i):
         n = int((row >= 0).sum())
         f[b] = dict(r=int(tr["r"][b - 1, i]) if b in cfg["merges"] else 0,
                     merge=merge,
-                    exit=bool(b in cfg["exits"] and res["exit_block"][i] == b),
+                    exit=bool(b in cfg["exits"] and res["exit_block"][i] == b and
+                              (b < L or (delta[cfg["exits"].index(b)] < 1.0 and
+                                         tr["c"][b - 1, i] >= delta[cfg["exits"].index(b)]))),
                     ids=row[:n].tolist())
     return f
 
@@ -129,11 +144,12 @@ def check_samples(cfg, W, imgs, res, idx, delta=None, rho=1.0):
     Wp = fo.prepare_weights(W, mode)
     tol = logit_tol(cfg, rho)
     etol = exit_tol(cfg, rho)
+    ptol = prune_tol(cfg, rho)
     worst, adopted = 0.0, []
     for i in idx:
         out = fo.run_sample(imgs[i], Wp, cfg, mode, delta=delta, rho=rho,
-                            follow=follow_of(cfg, res, i),
-                            tol={"exit": etol, "other": fo.TOL})
+                            follow=follow_of(cfg, res, i, delta),
+                            tol={"exit": etol, "other": fo.TOL, "prune": ptol})
         assert out["exit_block"] == res["exit_block"][i], i
         assert np.array_equal(out["token_counts"], res["counts"][i]), (
             i, out["token_counts"], res["counts"][i])

@@ -1,0 +1,95 @@
+"""GPU parity of the paper-faithful instantiation (Tab. I layer sets, merge
+ratios of Sec. III-C with Eq. 5, learned pruning scorer of Eq. 8, CLS and
+SpatialPool 2-layer MLP exit heads) with the CPU oracle, through the C ABI.
+
+Same rules as the other parity tests: decisions identical except near ties
+inside the decision margins, logits within 1e-4 (fp32) or the bf16 bound
+(2e-2, raised to 2.5x the contract's noise floor where larger)."""
+import numpy as np
+import pytest
+
+import parity_utils as pu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _report(tag, worst, adopted, n, res, cfg):
+    exits = np.bincount(res["exit_block"], minlength=cfg["L"] + 1)
+    print(f"[{tag}] samples={n} max|dlogit|={worst:.3e} near-tie adoptions="
+          f"{len(adopted)} exit blocks={ {b: int(exits[b]) for b in np.nonzero(exits)[0]} }",
+          flush=True)
+
+
+# thresholds that split the batch between the heads (the random-affine
+# heads are sharper at block 2 and flatter at block 3)
+@pytest.mark.parametrize("affine,router_std,rho,delta", [
+    ("plain", 0.02, 1.0, (0.5, 0.6)),
+    ("random", 0.5, 1.0, (0.74, 0.205)),
+    ("plain", 0.02, 1.5, (0.5, 0.6)),
+    ("random", 0.5, 0.5, (0.74, 0.205))])
+def test_tiny_paper_fp32_all_samples(torch_cuda, affine, router_std, rho, delta):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("tiny_paper", affine=affine, router_std=router_std)
+    print(f"[tiny_paper fp32] affine={affine} router_std={router_std} rho={rho} "
+          f"delta={delta}", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=list(delta), rho=rho)
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]),
+                                      delta=list(delta), rho=rho)
+    _report("tiny_paper", worst, adopted, cfg["batch"], res, cfg)
+    # the exit mix covers both heads and the final head
+    assert len(set(res["exit_block"].tolist())) >= 2
+
+
+def test_deit_s_paper_fp32_small_batch(torch_cuda):
+    """DeiT-S shape on the fp32 path (head gain 6 keeps the logits O(10))."""
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_s_paper", batch=8, precision="fp32", exit_gain=6.0)
+    print("[deit_s_paper fp32 b8]", flush=True)
+    m = pu.gpu_model(cfg, W, 8)
+    for delta in ([1.0, 1.0], [0.3, 0.5]):
+        res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=delta)
+        worst, adopted = pu.check_samples(cfg, W, imgs, res, range(8), delta=delta)
+        _report(f"deit_s_paper fp32 delta={delta}", worst, adopted, 8, res, cfg)
+
+
+@pytest.mark.parametrize("delta", [(0.8, 0.95), (1.0, 1.0)])
+def test_deit_s_paper_full_batch_sampled(torch_cuda, delta):
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_s_paper")
+    print(f"[deit_s_paper b256] delta={delta}", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=list(delta))
+    # samples that reach the prune blocks are the ones to check first
+    late = [i for i in range(cfg["batch"]) if res["exit_block"][i] > 8]
+    idx = sorted(set([0, 128, 255] + late[:3]))
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, idx, delta=list(delta))
+    _report("deit_s_paper", worst, adopted, len(idx), res, cfg)
+    if delta == (1.0, 1.0):
+        assert (res["exit_block"] == cfg["L"]).all()
+        # tokens: 197 -> three merges -> two prunes at keep 0.7
+        assert (res["counts"][:, 11] < res["counts"][:, 8]).all()
+
+
+def test_tiny_paper_empty_pool_after_full_prune(torch_cuda):
+    """rho = 4 merges every pair it can and prunes every patch token at block
+    3 (tau' = max(0, 1 - 4 * 0.3) = 0), so the pooled head at block 4 sees
+    CLS alone and pools the zero vector."""
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("tiny_paper", affine="random",
+                           exits=(2, 4), exit_kind=("cls_mlp", "pool_mlp"), delta=(1.0, 1.0))
+    print("[tiny_paper fp32] empty pool, rho=4", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[1.0, 1.0], rho=4.0)
+    assert (res["counts"][:, 3] == 1).all()
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]),
+                                      delta=[1.0, 1.0], rho=4.0)
+    _report("tiny_paper empty pool", worst, adopted, cfg["batch"], res, cfg)

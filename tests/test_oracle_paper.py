@@ -291,3 +291,18 @@ def test_blob_header_carries_rules():
     assert (mr, pr, hx) == (1, 1, 768)
     assert kinds[7] == 2 and kinds[9] == 1 and sum(kinds) == 3
     assert nt == len(weights.tensor_specs(cfg))
+
+
+def test_full_prune_leaves_cls_and_empty_pool():
+    """tau' = 0 at rho = 4 keeps no patch token; a pooled head after that
+    pools the zero vector, whose LayerNorm is the LN bias."""
+    cfg = configs.get("tiny_paper", exits=(2, 4), exit_kind=("cls_mlp", "pool_mlp"))
+    W = weights.make_weights(cfg, affine="random")
+    Wp = fo.prepare_weights(W, "fp32")
+    img = images.make_images(cfg, batch=1)
+    out = fo.run_sample(img[0], Wp, cfg, "fp32", delta=(1.0, 1.0), rho=4.0)
+    assert out["token_counts"][3] == 1
+    W4 = {k[len("blk4."):]: v for k, v in Wp.items() if k.startswith("blk4.")}
+    y = W4["eln_b"][None, :]
+    ref = (fo.gelu(y @ W4["ew1"].T + W4["eb1"]) @ W4["ew2"].T + W4["eb2"])[0]
+    np.testing.assert_allclose(out["trace"][4]["exit_logits"], ref, rtol=1e-6, atol=1e-6)
