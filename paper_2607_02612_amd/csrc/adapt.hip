@@ -486,7 +486,7 @@ hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
 // --------------------------------------------------------- compaction --
 // Grid: (live sample, part); every workgroup of a sample recomputes the
 // sample's offsets (cheap scans) and moves one contiguous range of its rows.
-constexpr int CP_PARTS = 4;
+constexpr int CP_PARTS = 8;
 template <typename T>
 __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   const int i = blockIdx.x, part = blockIdx.y;

@@ -154,7 +154,7 @@ __device__ __forceinline__ void wait_vm() {
 // MB = 256 (8 waves, 4x2), 128 (4 waves, 2x2) or 64 (2 waves, 1x2) rows per
 // tile.  KSV = K step.
 template <int EPI, int MB, int KSV>
-__global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
+__global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
     int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
   constexpr int KS = KSV, NSTG = KSV == 64 ? 2 : 3;
@@ -258,23 +258,30 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
     // bf16 tile -> LDS (256-byte rows, 16-byte chunk c stored at c ^ (row % 16))
     // -> global, 16 lanes per 256-byte row segment
     __syncthreads();
+    // the four bias vectors of a column block are loaded together (columns
+    // clamped into range, so no branch separates the loads from each other)
 #pragma unroll
-    for (int i = 0; i < 2; i++) {
-      const int r = wm * 64 + i * 32 + (lane & 31);
+    for (int j = 0; j < 2; j++) {
+      float4 bv[4];
 #pragma unroll
-      for (int j = 0; j < 2; j++) {
+      for (int q4 = 0; q4 < 4; q4++) {
+        const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
+        bv[q4] = *(const float4*)(e.bias + min(n0 + c, N - 4));
+      }
+#pragma unroll
+      for (int i = 0; i < 2; i++) {
+        const int r = wm * 64 + i * 32 + (lane & 31);
 #pragma unroll
         for (int q4 = 0; q4 < 4; q4++) {
           const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
-          if (n0 + c >= N) continue;
-          const float4 bv = *(const float4*)(e.bias + n0 + c);
-          float v0 = acc[i][j][4 * q4 + 0] + bv.x, v1 = acc[i][j][4 * q4 + 1] + bv.y;
-          float v2 = acc[i][j][4 * q4 + 2] + bv.z, v3 = acc[i][j][4 * q4 + 3] + bv.w;
+          float v0 = acc[i][j][4 * q4 + 0] + bv[q4].x, v1 = acc[i][j][4 * q4 + 1] + bv[q4].y;
+          float v2 = acc[i][j][4 * q4 + 2] + bv[q4].z, v3 = acc[i][j][4 * q4 + 3] + bv[q4].w;
           if (EPI == EPI_GELU) {
             v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
           }
           const uint2 pk = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
-          *(uint2*)(smem + r * (NB * 2) + (((c >> 3) ^ (r & 15)) << 4) + ((c >> 2) & 1) * 8) = pk;
+          if (n0 + c < N)
+            *(uint2*)(smem + r * (NB * 2) + (((c >> 3) ^ (r & 15)) << 4) + ((c >> 2) & 1) * 8) = pk;
         }
       }
     }
@@ -305,24 +312,29 @@ __global__ __launch_bounds__(MB / 64 * 128) void gemm_mfma_bf16(
     }
 #pragma unroll
     for (int j = 0; j < 2; j++) {
+      // all loads of the column block first (bias, and the residual or
+      // position rows), then the arithmetic and the stores
+      float4 bv[4], xv[4];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; q4++) {
+        const int nb = min(n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5), N - 4);
+        bv[q4] = *(const float4*)(e.bias + nb);
+        if (EPI == EPI_RESID) xv[q4] = *(const float4*)((const float*)e.out + orow * e.ldo + nb);
+        if (EPI == EPI_PATCH) xv[q4] = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + nb);
+      }
 #pragma unroll
       for (int q4 = 0; q4 < 4; q4++) {
         const int nb = n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
         if (nb >= N) continue;
-        const float4 bv = *(const float4*)(e.bias + nb);
-        const float v0 = acc[i][j][4 * q4 + 0] + bv.x, v1 = acc[i][j][4 * q4 + 1] + bv.y;
-        const float v2 = acc[i][j][4 * q4 + 2] + bv.z, v3 = acc[i][j][4 * q4 + 3] + bv.w;
+        const float v0 = acc[i][j][4 * q4 + 0] + bv[q4].x, v1 = acc[i][j][4 * q4 + 1] + bv[q4].y;
+        const float v2 = acc[i][j][4 * q4 + 2] + bv[q4].z, v3 = acc[i][j][4 * q4 + 3] + bv[q4].w;
+        float4* po = (float4*)((float*)e.out + orow * e.ldo + nb);
         if (EPI == EPI_RESID) {
-          float4* px = (float4*)((float*)e.out + orow * e.ldo + nb);
-          float4 xv = *px;
-          xv.x = xv.x + v0; xv.y = xv.y + v1; xv.z = xv.z + v2; xv.w = xv.w + v3;
-          *px = xv;
+          *po = make_float4(xv[q4].x + v0, xv[q4].y + v1, xv[q4].z + v2, xv[q4].w + v3);
         } else if (EPI == EPI_F32) {
-          *(float4*)((float*)e.out + orow * e.ldo + nb) = make_float4(v0, v1, v2, v3);
+          *po = make_float4(v0, v1, v2, v3);
         } else {  // EPI_PATCH: + position embedding of token 1 + pj
-          const float4 pv = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + nb);
-          *(float4*)((float*)e.out + orow * e.ldo + nb) =
-              make_float4(v0 + pv.x, v1 + pv.y, v2 + pv.z, v3 + pv.w);
+          *po = make_float4(v0 + xv[q4].x, v1 + xv[q4].y, v2 + xv[q4].z, v3 + xv[q4].w);
         }
       }
     }
