@@ -351,30 +351,38 @@ __global__ __launch_bounds__(RES_NT, 4) void attention_mfma_res(AttnArgs a) {
   constexpr int KU = (TP * 8 + RES_NT - 1) / RES_NT;  // 16-byte K pieces per thread
   const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
   const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
+  // (rows past the sample read its last row and are replaced by zeros
+  // afterwards, so no load sits behind a branch and they issue together)
   uint4 kin[KU];
 #pragma unroll
   for (int w = 0; w < KU; w++) {
     const int u = tid + w * RES_NT;
     const int r = u >> 3, cc = (u & 7) * 8;
-    kin[w] = make_uint4(0, 0, 0, 0);
-    if (u < TP * 8 && r < Tn) kin[w] = *(const uint4*)(kg + (size_t)r * ld + cc);
+    kin[w] = *(const uint4*)(kg + (size_t)min(r, Tn - 1) * ld + cc);
   }
   // V^T: thread = 4 keys x 8 dims block, transposed in registers
   const int kb = tid >> 3, db = (tid & 7) * 8;   // keys 4kb.., dims db..
   const bool vth = tid < 2 * TPE;
-  uint32_t in[4][4];
+  uint4 vin[4];
 #pragma unroll
-  for (int r = 0; r < 4; r++) {
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (vth && kb * 4 + r < Tn) v = *(const uint4*)(vg + (size_t)(kb * 4 + r) * ld + db);
-    in[r][0] = v.x; in[r][1] = v.y; in[r][2] = v.z; in[r][3] = v.w;
-  }
-  const float sz = (tid < Tn && a.prop_attn) ? a.size[base + tid] : 1.f;
+  for (int r = 0; r < 4; r++)
+    vin[r] = *(const uint4*)(vg + (size_t)min(kb * 4 + r, Tn - 1) * ld + db);
+  const float szr = a.size[base + min(tid, Tn - 1)];
+  __builtin_amdgcn_sched_barrier(0);  // every load above is in flight before any use
 #pragma unroll
   for (int w = 0; w < KU; w++) {
     const int u = tid + w * RES_NT;
-    if (u < TP * 8) *(uint4*)(Ks + (u >> 3) * 64 + (((u & 7) ^ ((u >> 3) & 7)) << 3)) = kin[w];
+    if (u < TP * 8)
+      *(uint4*)(Ks + (u >> 3) * 64 + (((u & 7) ^ ((u >> 3) & 7)) << 3)) =
+          (u >> 3) < Tn ? kin[w] : make_uint4(0, 0, 0, 0);
   }
+  uint32_t in[4][4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    const uint4 v = (vth && kb * 4 + r < Tn) ? vin[r] : make_uint4(0, 0, 0, 0);
+    in[r][0] = v.x; in[r][1] = v.y; in[r][2] = v.z; in[r][3] = v.w;
+  }
+  const float sz = (tid < Tn && a.prop_attn) ? szr : 1.f;
   if (vth) {
 #pragma unroll
     for (int j = 0; j < 8; j++) {
