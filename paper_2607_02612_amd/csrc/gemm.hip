@@ -296,8 +296,65 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
     }
     return;
   }
-  // residual update, fp32 logits (row scatter) and the patch embedding:
-  // direct vector accesses
+  if (EPI == EPI_RESID && MB == 128) {
+    // residual update through LDS: (acc + bias) rows are staged in fp32
+    // (512-byte rows, 16-byte chunk c of row r at c ^ (r % 32)), then the
+    // workgroup adds them to x with whole-row accesses (32 lanes per
+    // 512-byte row segment) instead of 16-byte pieces of 32 rows per
+    // instruction.  RR rows per round: all 128 when the drained ring holds
+    // 64 KB (K step 64), else two rounds of 64.
+    constexpr int RR = NSTG * STGB >= MB * NB * 4 ? MB : 64;
+    float* x = (float*)e.out;
+#pragma unroll
+    for (int rb = 0; rb < MB; rb += RR) {
+      __syncthreads();
+      if (wm * 64 >= rb && wm * 64 < rb + RR) {
+#pragma unroll
+        for (int j = 0; j < 2; j++) {
+          float4 bv[4];
+#pragma unroll
+          for (int q4 = 0; q4 < 4; q4++) {
+            const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
+            bv[q4] = *(const float4*)(e.bias + min(n0 + c, N - 4));
+          }
+#pragma unroll
+          for (int i = 0; i < 2; i++) {
+            const int r = wm * 64 + i * 32 + (lane & 31) - rb;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; q4++) {
+              const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
+              *(float4*)(smem + r * (NB * 4) + (((c >> 2) ^ (r & 31)) << 4)) =
+                  make_float4(acc[i][j][4 * q4 + 0] + bv[q4].x, acc[i][j][4 * q4 + 1] + bv[q4].y,
+                              acc[i][j][4 * q4 + 2] + bv[q4].z, acc[i][j][4 * q4 + 3] + bv[q4].w);
+            }
+          }
+        }
+      }
+      __syncthreads();
+      constexpr int PER = RR * (NB / 4) / NT;          // 16-byte pieces per thread
+      float4 xv[PER];
+#pragma unroll
+      for (int k = 0; k < PER; k++) {
+        const int idx = tid + k * NT;
+        const int r = idx / (NB / 4), ch = idx % (NB / 4);
+        const int m = min(m0 + rb + r, M - 1), n = min(n0 + ch * 4, N - 4);
+        xv[k] = *(const float4*)(x + (size_t)m * e.ldo + n);
+      }
+#pragma unroll
+      for (int k = 0; k < PER; k++) {
+        const int idx = tid + k * NT;
+        const int r = idx / (NB / 4), ch = idx % (NB / 4);
+        const int m = m0 + rb + r, n = n0 + ch * 4;
+        const float4 sv = *(const float4*)(smem + r * (NB * 4) + ((ch ^ (r & 31)) << 4));
+        if (m < M && n < N)
+          *(float4*)(x + (size_t)m * e.ldo + n) =
+              make_float4(xv[k].x + sv.x, xv[k].y + sv.y, xv[k].z + sv.z, xv[k].w + sv.w);
+      }
+    }
+    return;
+  }
+  // residual update (other tile heights), fp32 logits (row scatter) and the
+  // patch embedding: direct vector accesses
 #pragma unroll
   for (int i = 0; i < 2; i++) {
     const int m = m0 + wm * 64 + i * 32 + (lane & 31);
