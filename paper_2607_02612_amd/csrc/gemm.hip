@@ -296,8 +296,9 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
     }
     return;
   }
-  if (EPI == EPI_RESID && MB == 128) {
-    // residual update through LDS: (acc + bias) rows are staged in fp32
+  if ((EPI == EPI_RESID || EPI == EPI_PATCH) && MB <= 128) {
+    // residual update (and patch embedding) through LDS: (acc + bias) rows
+    // are staged in fp32
     // (512-byte rows, 16-byte chunk c of row r at c ^ (r % 32)), then the
     // workgroup adds them to x with whole-row accesses (32 lanes per
     // 512-byte row segment) instead of 16-byte pieces of 32 rows per
@@ -332,13 +333,21 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
       }
       __syncthreads();
       constexpr int PER = RR * (NB / 4) / NT;          // 16-byte pieces per thread
+      // the addend: the residual row (x += ...) or, for the patch
+      // embedding, the position embedding of patch token 1 + j, whose
+      // output row is s (n0 + 1) + 1 + j for packed row r = s n0 + j
       float4 xv[PER];
 #pragma unroll
       for (int k = 0; k < PER; k++) {
         const int idx = tid + k * NT;
         const int r = idx / (NB / 4), ch = idx % (NB / 4);
         const int m = min(m0 + rb + r, M - 1), n = min(n0 + ch * 4, N - 4);
-        xv[k] = *(const float4*)(x + (size_t)m * e.ldo + n);
+        if (EPI == EPI_RESID) {
+          xv[k] = *(const float4*)(x + (size_t)m * e.ldo + n);
+        } else {
+          const int pj = m - (m / e.n0) * e.n0;
+          xv[k] = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + n);
+        }
       }
 #pragma unroll
       for (int k = 0; k < PER; k++) {
@@ -346,9 +355,15 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
         const int r = idx / (NB / 4), ch = idx % (NB / 4);
         const int m = m0 + rb + r, n = n0 + ch * 4;
         const float4 sv = *(const float4*)(smem + r * (NB * 4) + ((ch ^ (r & 31)) << 4));
-        if (m < M && n < N)
-          *(float4*)(x + (size_t)m * e.ldo + n) =
-              make_float4(xv[k].x + sv.x, xv[k].y + sv.y, xv[k].z + sv.z, xv[k].w + sv.w);
+        if (m < M && n < N) {
+          size_t orow = (size_t)m;
+          if (EPI == EPI_PATCH) {
+            const int sidx = m / e.n0;
+            orow = (size_t)sidx * (e.n0 + 1) + 1 + (m - sidx * e.n0);
+          }
+          *(float4*)(x + orow * e.ldo + n) =
+              make_float4(sv.x + xv[k].x, sv.y + xv[k].y, sv.z + xv[k].z, sv.w + xv[k].w);
+        }
       }
     }
     return;
