@@ -136,6 +136,9 @@ constexpr int NXCD = 8;
 #ifndef GEMM_BIG_TILES
 #define GEMM_BIG_TILES 1
 #endif
+#ifndef GEMM_K64_MIN
+#define GEMM_K64_MIN 1024
+#endif
 
 template <int KSV>
 __device__ __forceinline__ int kslot(int r, int c) {
@@ -443,7 +446,7 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   const bool small = (long)((M_ub + 127) / 128) * n_nt < 512;
   // long K on 128-row tiles: 64-wide K steps (half the barriers); otherwise
   // 32-wide steps with three stages
-  const bool k64 = !small && K % 64 == 0 && K >= 1024;
+  const bool k64 = !small && K % 64 == 0 && K >= GEMM_K64_MIN;
   const bool big = !k64 && GEMM_BIG_TILES && (long)((M_ub + 255) / 256) * n_nt >= 1024;
   const int mb = small ? 64 : big ? 256 : 128;
   const int n_mt = (M_ub + mb - 1) / mb;
