@@ -447,7 +447,10 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   // long K on 128-row tiles: 64-wide K steps (half the barriers); otherwise
   // 32-wide steps with three stages
   const bool k64 = !small && K % 64 == 0 && K >= GEMM_K64_MIN;
-  const bool big = !k64 && GEMM_BIG_TILES && (long)((M_ub + 255) / 256) * n_nt >= 1024;
+  // (not for the GELU epilogue, whose vector work overlaps better with
+  // three 4-wave workgroups per CU than with two 8-wave ones)
+  const bool big = !k64 && GEMM_BIG_TILES && e.mode != EPI_GELU &&
+                   (long)((M_ub + 255) / 256) * n_nt >= 1024;
   const int mb = small ? 64 : big ? 256 : 128;
   const int n_mt = (M_ub + mb - 1) / mb;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
