@@ -118,10 +118,12 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // clamped to the last valid row for the loads (every address stays in
 // bounds) and masked in the epilogue.
 //
-// Epilogue: bf16 outputs are staged through LDS (the drained K ring) so
+// Epilogue: every load it needs (bias, residual or position rows) is issued
+// as one batch.  bf16 outputs are staged through LDS (the drained K ring) so
 // that global stores are whole 256-byte row segments instead of 16-byte
-// pieces of 32 different rows; the fp32 residual update reads and writes x
-// directly (16 bytes per lane).
+// pieces of 32 different rows; the fp32 residual update and the patch
+// embedding are staged the same way as fp32 rows (512-byte segments), on
+// tiles of up to 128 rows; fp32 logits and 256-row tiles write directly.
 //
 // Tile order: blocks are dispatched round-robin over the 8 XCDs (block id %
 // 8); the linear id is remapped so that each XCD walks whole row panels (all
