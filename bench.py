@@ -73,30 +73,47 @@ def dense_flops(cfg):
 
 
 def kernel_work(cfg, counts):
-    """Algorithmic FLOPs (matrix kernels) or bytes (memory-bound kernels) of
-    every launch kind over one step, from the token counts."""
+    """Algorithmic FLOPs and bytes of every launch kind over one step, from
+    the token counts: each operand read once, each output written once (the
+    fp32 residual stream read and written by the residual GEMMs).  Returns
+    {kind: {"flop": F, "byte": B, "launches": n}}."""
     d, mlp, H = cfg["d"], cfg["mlp"], cfg["H"]
     T = counts.astype(np.float64)
     live = T > 0
     M = T.sum(axis=0)                       # rows per block
-    ns = live.sum(axis=0)                   # live samples per block
+    nb = float((M > 0).sum())               # blocks run (one launch each)
+    B, N0, pd = counts.shape[0], cfg["N0"], cfg["patch_dim"]
     w = {
-        "gemm_qkv": ("flop", float((2 * M * d * 3 * d).sum())),
-        "gemm_proj": ("flop", float((2 * M * d * d).sum())),
-        "gemm_fc1_gelu": ("flop", float((2 * M * d * mlp).sum())),
-        "gemm_fc2": ("flop", float((2 * M * mlp * d).sum())),
-        "attention": ("flop", float((4 * T * T * d).sum())),
-        "patch_embed": ("flop", 2.0 * counts.shape[0] * cfg["N0"] * cfg["patch_dim"] * d),
+        "gemm_qkv": {"flop": float((2 * M * d * 3 * d).sum()),
+                     "byte": float((M * d * 2 + M * 3 * d * 2).sum() + nb * 3 * d * d * 2)},
+        "gemm_proj": {"flop": float((2 * M * d * d).sum()),
+                      "byte": float((M * d * 2 + M * d * 8).sum() + nb * d * d * 2)},
+        "gemm_fc1_gelu": {"flop": float((2 * M * d * mlp).sum()),
+                          "byte": float((M * d * 2 + M * mlp * 2).sum() + nb * mlp * d * 2)},
+        "gemm_fc2": {"flop": float((2 * M * mlp * d).sum()),
+                     "byte": float((M * mlp * 2 + M * d * 8).sum() + nb * d * mlp * 2)},
+        # q, k, v read once (bf16), the output written once (bf16)
+        "attention": {"flop": float((4 * T * T * d).sum()),
+                      "byte": float((T * 3 * d * 2 + T * d * 2).sum())},
+        "patch_embed": {"flop": 2.0 * B * N0 * pd * d,
+                        "byte": B * N0 * (pd * 4 + pd * 2 + pd * 2 + d * 4) + d * pd * 2.0},
         # LayerNorm kernel: read fp32 rows, write bf16 rows; LN2 of every
         # block and LN1 of block 1 (later LN1s are written by the compaction)
-        "layernorm": ("byte", float((M * d * (4 + 2)).sum() + M[0] * d * (4 + 2))),
+        "layernorm": {"flop": 0.0, "byte": float((M * d * (4 + 2)).sum() + M[0] * d * (4 + 2))},
+        # adapt: read the sample's fp32 rows and sizes, write the merged rows
+        # back; compaction after block b: read and write the rows kept for
+        # block b + 1 (x, size, origin) and write their LN1 (bf16)
+        "adapt": {"flop": 0.0, "byte": float((M * (d * 4 + 8) * 2).sum())},
+        "compact": {"flop": 0.0, "byte": float((M[1:] * ((d * 4 + 8) * 2 + d * 2)).sum())},
     }
-    # adapt: read the sample's fp32 rows and sizes, write the merged rows
-    # back; compaction after block b: read and write the rows kept for block
-    # b + 1 (x, size, origin) and write their LN1 (bf16)
-    w["adapt"] = ("byte", float((M * (d * 4 + 8) * 2).sum()))
-    w["compact"] = ("byte", float((M[1:] * ((d * 4 + 8) * 2 + d * 2)).sum()))
     return w
+
+
+def roofline_bound(work):
+    """The roofline resource of a launch kind: "mfma" when its FLOPs take
+    longer at the dense bf16 peak than its bytes at the HBM peak, else
+    "hbm"."""
+    return "mfma" if work["flop"] / BF16_PEAK >= work["byte"] / HBM_PEAK else "hbm"
 
 
 def measured_traffic(kernel):
@@ -470,21 +487,38 @@ def main():
             continue
         entry = {"ms_per_step": ms_tot / args.steps, "launches_per_step": n / args.steps}
         if k in work:
-            kind, amount = work[k]
-            rate = amount / (ms_tot / args.steps / 1e3)
-            if kind == "flop":
-                entry["tflops"] = rate / 1e12
-                entry["frac_bf16_peak"] = rate / BF16_PEAK
-            else:
-                entry["gbps"] = rate / 1e9
-                entry["frac_hbm_peak"] = rate / HBM_PEAK
+            sec = ms_tot / args.steps / 1e3
+            wk = work[k]
+            if wk["flop"] > 0:
+                entry["tflops"] = wk["flop"] / sec / 1e12
+                entry["frac_bf16_peak"] = wk["flop"] / sec / BF16_PEAK
+            entry["gbps"] = wk["byte"] / sec / 1e9
+            entry["frac_hbm_peak"] = wk["byte"] / sec / HBM_PEAK
+            entry["roofline_bound"] = roofline_bound(wk)
         kernels[k] = entry
-    flop_kernels = {k: v for k, v in kernels.items() if "tflops" in v}
-    dom = max(flop_kernels, key=lambda k: flop_kernels[k]["ms_per_step"])
+    # the dominant kernel (most time per step among those with an algorithmic
+    # work model), reported against the peak of its roofline resource
+    dom = max((k for k in kernels if "roofline_bound" in kernels[k]),
+              key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
-    roofline = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
-                "peak": BF16_PEAK / 1e12, "unit": "TFLOP/s",
-                "frac": dk["frac_bf16_peak"], "traffic": measured_traffic(dom)}
+    if dk["roofline_bound"] == "mfma":
+        roofline = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
+                    "peak": BF16_PEAK / 1e12, "unit": "TFLOP/s",
+                    "frac": dk["frac_bf16_peak"], "traffic": measured_traffic(dom)}
+    else:
+        roofline = {"kernel": dom, "bound": "hbm", "achieved": dk["gbps"],
+                    "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                    "frac": dk["frac_hbm_peak"], "traffic": measured_traffic(dom)}
+    if "tflops" in dk:
+        roofline["mfma_tflops"] = dk["tflops"]
+        roofline["frac_bf16_peak"] = dk["frac_bf16_peak"]
+    # the whole step on the roofline: executed FLOPs at the MFMA peak against
+    # the algorithmic bytes of all kinds at the HBM peak
+    step_bytes = sum(w["byte"] for w in work.values())
+    step_roof = {"executed_gflop": head["flops"] / 1e9, "algorithmic_gbytes": step_bytes / 1e9,
+                 "ms_at_mfma_peak": head["flops"] / BF16_PEAK * 1e3,
+                 "ms_at_hbm_peak": step_bytes / HBM_PEAK * 1e3,
+                 "ms_measured": head["ms"]}
 
     line = {
         "metric": "images/sec at DeiT-S b=256 bf16 (1 GPU); % bf16 MFMA peak on executed FLOPs",
@@ -508,6 +542,7 @@ def main():
                                              "executed_gflop_per_image": r["flops"] / B / 1e9}
                        for e, r in sweep.items()},
         "roofline": roofline,
+        "step_roofline": step_roof,
         "kernels": kernels,
     }
     if not (args.no_paper or args.headline_only):
