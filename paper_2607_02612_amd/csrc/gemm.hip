@@ -138,9 +138,6 @@ constexpr int NXCD = 8;
 #ifndef GEMM_BIG_TILES
 #define GEMM_BIG_TILES 1
 #endif
-#ifndef GEMM_K64_MIN
-#define GEMM_K64_MIN 1024
-#endif
 
 template <int KSV>
 __device__ __forceinline__ int kslot(int r, int c) {
@@ -446,12 +443,11 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   // tile rows: 256 (8 waves) when there are enough tiles to fill the CUs
   // several times over, 64 when 128-row tiles would leave CUs idle
   const bool small = (long)((M_ub + 127) / 128) * n_nt < 512;
-  // long K on 128-row tiles: 64-wide K steps (half the barriers); otherwise
-  // 32-wide steps with three stages
-  const bool k64 = !small && K % 64 == 0 && K >= GEMM_K64_MIN;
+  // K steps of 32 with three stages everywhere: 64-wide steps (two stages,
+  // half the barriers) measured slower on every shape here, long K included
   // (not for the GELU epilogue, whose vector work overlaps better with
   // three 4-wave workgroups per CU than with two 8-wave ones)
-  const bool big = !k64 && GEMM_BIG_TILES && e.mode != EPI_GELU &&
+  const bool big = GEMM_BIG_TILES && e.mode != EPI_GELU &&
                    (long)((M_ub + 255) / 256) * n_nt >= 1024;
   const int mb = small ? 64 : big ? 256 : 128;
   const int n_mt = (M_ub + mb - 1) / mb;
@@ -459,8 +455,6 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
 #define FUSION_GEMM_LAUNCH(E)                                                                 \
   if (small)                                                                                 \
     gemm_mfma_bf16<E, 64, 32><<<grid, 128, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
-  else if (k64)                                                                              \
-    gemm_mfma_bf16<E, 128, 64><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
   else if (big)                                                                              \
     gemm_mfma_bf16<E, 256, 32><<<grid, 512, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
   else                                                                                       \
