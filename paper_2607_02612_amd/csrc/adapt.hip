@@ -14,19 +14,22 @@ namespace fusion {
 
 constexpr int AD_TMAX = 640;  // tokens per sample (CLS included), largest size class
 constexpr int AD_NT = 512;    // threads per workgroup (8 waves)
-constexpr int SAG = 128;      // A rows per pass: one 16-row MFMA tile per wave
 
 // Size classes of the per-sample kernel: TMAX tokens (CLS included), so
-// |A| = ceil(N/2) and |B| = floor(N/2) are at most TMAX/2; the similarity
-// features are staged in chunks of SKC (64 for the small class: fewer
-// round trips to memory; 32 for the large one, whose B tiles fill the LDS).
+// |A| = ceil(N/2) and |B| = floor(N/2) are at most TMAX/2.
 template <int TMAX_> struct AdSize {
   static constexpr int TMAX = TMAX_;
   static constexpr int AMAX = TMAX_ / 2;
   static constexpr int BMAX = TMAX_ / 2;
-  static constexpr int SKC = TMAX_ <= 256 ? 64 : 32;
+  static constexpr int SKC = 32;               // features per chunk (one MFMA K step)
   static constexpr int SKP = SKC + 8;          // padded LDS row (bf16)
-  static constexpr int NBT = BMAX / 16;        // B tiles held in registers
+  // similarity wave layout: WC column groups of B tiles, AD_NT / 64 / WC
+  // groups of 32 A rows; SAG A rows per pass
+  static constexpr int WC = TMAX_ <= 256 ? 2 : 4;
+  static constexpr int SAG = 32 * (AD_NT / 64 / WC);
+  static constexpr int NBT = BMAX / 16;        // B tiles of 16 rows
+  static constexpr int NBW = NBT / WC;         // B tiles per wave
+  static constexpr int BG = TMAX_ <= 256 ? 4 : 5;  // B tiles per group of the MFMA loop
   static constexpr int SPT = ((SAG + BMAX) * (SKC / 4) + AD_NT - 1) / AD_NT;  // slots / thread
 };
 
@@ -99,6 +102,14 @@ __device__ __forceinline__ int block_compact(bool f, int v, int* out, int* red) 
   return tot;
 }
 
+// Lanes that share one element's rank count when n elements are ranked by
+// the workgroup: the largest power of two (at most 16) with n * P <= AD_NT.
+__device__ __forceinline__ int rank_lanes(int n) {
+  int P = 1;
+  while (P < 16 && n * (2 * P) <= AD_NT) P *= 2;
+  return P;
+}
+
 // Split a float into bf16 hi + lo with hi + lo = v to about 2^-17 relative.
 __device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
   hi = f32_to_bf16(v);
@@ -108,144 +119,220 @@ __device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
 // Cosine similarities of the A tokens (even patch slots) with the B tokens
 // (odd slots) of one sample, and the best B for every A.
 //
-// One pass over the features in chunks of SKC: every thread stages a fixed
-// set of (row, 4-feature) slots, splits the fp32 values into bf16 hi + lo,
-// and accumulates the row's sum of squares on the way; the dot products
-// take hi.hi' + hi.lo' + lo.hi' on v_mfma_f32_16x16x32_bf16 with fp32
-// accumulation (absolute error of a cosine <= ~1.2e-5, the dropped lo.lo'
-// term included).  The loads of chunk k+1 are issued before the MFMAs of
-// chunk k.  At the end the dots are divided by the clamped norms
-// max(||x||, 1e-12) of both tokens.  Wave w owns A rows ag + 16w .. +15
-// against every B tile; lane l of an output tile holds S[a = 4(l/16) + j]
-// [b = l%16].
+// One pass over the features in chunks of SKC, double-buffered in LDS.
+// Every thread owns a fixed set of (row, 4-feature) slots: the A rows of the
+// pass first, then the B rows (addresses clamped to the last real row, so
+// the loads need no branch; padding rows only feed outputs that are never
+// read).  The loads run two chunks ahead in two register sets.  A chunk's
+// values are split into bf16 hi + lo (hi = RNE(v), lo = RNE(v - hi)), with
+// the row's sum of squares accumulated on the way, and written to the LDS
+// buffer that the MFMAs of the current chunk do not read: one barrier per
+// chunk.  The dot products take hi.hi' + hi.lo' + lo.hi' on
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation (absolute error of a
+// cosine <= ~1.2e-5, the dropped lo.lo' term included), per output in
+// feature order, the three terms in that order within each 32 features.
+// The B fragment is the MFMA's row operand, so lane l of a 16 x 16 output
+// tile holds S[b = 4 (l / 16) + j][a = l % 16] (j = 0..3): the candidates
+// of one A token sit in 4 lanes x 4 registers per B tile.  Wave w owns A
+// rows 32 (w / WC) .. +31 of the pass against B tiles NBW (w % WC) .. +NBW-1.
+// Cosines are dot * (1 / n_a) * (1 / n_b) with the clamped norms
+// max(||x||, 1e-12).  The argmax over B (ties to the lowest B index, NaN
+// never wins) runs in-lane, then across the 4 lanes of a token with the
+// lane-swap instructions, then over the WC wave groups in B order through
+// LDS (pbv, pbi: WC SAG entries each).  rn holds the reciprocal norms:
+// A rows of the pass at [0, SAG), B rows at [SAG, SAG + BMAX).
 template <class Z>
 __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
-                                  int nA, int nB, float* nrm, float* bestsim,
+                                  int nA, int nB, float* rn, float* bestsim,
                                   int* best, bf16_t* Ahi, bf16_t* Alo,
-                                  bf16_t* Bhi, bf16_t* Blo) {
-  constexpr int SKC = Z::SKC, SKP = Z::SKP, SPT = Z::SPT, NBT = Z::NBT;
+                                  bf16_t* Bhi, bf16_t* Blo, float* pbv, int* pbi) {
+  constexpr int SKC = Z::SKC, SKP = Z::SKP, SPT = Z::SPT, NBW = Z::NBW, BG = Z::BG;
+  constexpr int SAG = Z::SAG, WC = Z::WC, BMAX = Z::BMAX;
+  constexpr int Q = SKC / 4;  // 16-byte slots per row and chunk
+  static_assert(SKC == 32, "one MFMA K step per chunk");
+  static_assert(SPT * AD_NT == (SAG + BMAX) * Q, "slots must tile the staged rows exactly");
+  static_assert(NBW % BG == 0 && NBW * WC == Z::NBT, "wave layout: B tiles split evenly");
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, c = lane & 15;
-  const int nbt = (nB + 15) >> 4;
-  const int nslot = (SAG + nbt * 16) * (SKC / 4);
+  const int wr = wave / WC, wc = wave % WC;
+  const int nbt = (nB + 15) >> 4, nck = d / SKC;
   for (int ag = 0; ag < nA; ag += SAG) {
-    // this thread's slots: row r = u / (SKC/4) (A rows first, then B rows)
-    const float* srow[SPT];
+    const float* xs = x + (size_t)base * d;
+    int soff[SPT];  // slot offsets from the sample's first row, in floats
+    bool sval[SPT];
     float ss[SPT];
 #pragma unroll
     for (int w = 0; w < SPT; w++) {
       const int u = tid + w * AD_NT;
-      const int r = u / (SKC / 4), q = (u % (SKC / 4)) * 4;
-      srow[w] = nullptr;
-      ss[w] = 0.f;
-      if (u < nslot) {
-        if (r < SAG) {
-          if (ag + r < nA) srow[w] = x + (size_t)(base + 1 + 2 * (ag + r)) * d + q;
-        } else if (r - SAG < nB) {
-          srow[w] = x + (size_t)(base + 2 + 2 * (r - SAG)) * d + q;
-        }
+      const int r = u / Q, q = (u % Q) * 4;
+      if (r < SAG) {
+        sval[w] = ag + r < nA;
+        soff[w] = (1 + 2 * min(ag + r, nA - 1)) * d + q;
+      } else {
+        sval[w] = r - SAG < nB;
+        soff[w] = (2 + 2 * min(r - SAG, nB - 1)) * d + q;
       }
+      ss[w] = 0.f;
     }
-    float4 cur[SPT];
+    auto load = [&](float4(&cx)[SPT], int kc) {
 #pragma unroll
-    for (int w = 0; w < SPT; w++)
-      cur[w] = srow[w] ? *(const float4*)srow[w] : make_float4(0.f, 0.f, 0.f, 0.f);
-    f32x4_t acc[NBT];
-#pragma unroll
-    for (int t = 0; t < NBT; t++) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < d; k0 += SKC) {
-      __syncthreads();
+      for (int w = 0; w < SPT; w++) cx[w] = *(const float4*)(xs + soff[w] + kc * SKC);
+    };
+    // split chunk values into hi / lo and write them to LDS buffer `buf`
+    auto stage = [&](const float4(&cx)[SPT], int buf) {
 #pragma unroll
       for (int w = 0; w < SPT; w++) {
-        const int u = tid + w * AD_NT;
-        if (u >= nslot) continue;
-        const int r = u / (SKC / 4), q = (u % (SKC / 4)) * 4;
-        bf16_t* H = r < SAG ? Ahi + r * SKP : Bhi + (r - SAG) * SKP;
-        bf16_t* Lo = r < SAG ? Alo + r * SKP : Blo + (r - SAG) * SKP;
-        const float4 e = cur[w];
+        const float4 e = cx[w];
         ss[w] = fmaf(e.x, e.x, ss[w]);
         ss[w] = fmaf(e.y, e.y, ss[w]);
         ss[w] = fmaf(e.z, e.z, ss[w]);
         ss[w] = fmaf(e.w, e.w, ss[w]);
-        // hi = RNE(v), lo = RNE(v - hi): four values -> two 8-byte stores
         const uint32_t h01 = pack_bf16x2(e.x, e.y), h23 = pack_bf16x2(e.z, e.w);
-        const uint32_t l01 = pack_bf16x2(e.x - __uint_as_float(h01 << 16),
-                                         e.y - __uint_as_float(h01 & 0xFFFF0000u));
-        const uint32_t l23 = pack_bf16x2(e.z - __uint_as_float(h23 << 16),
-                                         e.w - __uint_as_float(h23 & 0xFFFF0000u));
-        *(uint2*)(H + q) = make_uint2(h01, h23);
-        *(uint2*)(Lo + q) = make_uint2(l01, l23);
+        const uint2 hv = make_uint2(h01, h23);
+        const uint2 lv = make_uint2(pack_bf16x2(e.x - __uint_as_float(h01 << 16),
+                                                e.y - __uint_as_float(h01 & 0xFFFF0000u)),
+                                    pack_bf16x2(e.z - __uint_as_float(h23 << 16),
+                                                e.w - __uint_as_float(h23 & 0xFFFF0000u)));
+        const int u = tid + w * AD_NT;
+        const int r = u / Q, q = (u % Q) * 4;
+        bf16_t* H = r < SAG ? Ahi + (buf * SAG + r) * SKP : Bhi + (buf * BMAX + r - SAG) * SKP;
+        bf16_t* Lo = r < SAG ? Alo + (buf * SAG + r) * SKP : Blo + (buf * BMAX + r - SAG) * SKP;
+        *(uint2*)(H + q) = hv;
+        *(uint2*)(Lo + q) = lv;
       }
-      // prefetch the next chunk while this one is multiplied
-      if (k0 + SKC < d) {
+    };
+    f32x4_t acc[2][NBW];
 #pragma unroll
-        for (int w = 0; w < SPT; w++)
-          if (srow[w]) cur[w] = *(const float4*)(srow[w] + k0 + SKC);
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+      for (int t = 0; t < NBW; t++) acc[i][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // wave-uniform: does this wave's block hold any real (A, B) pair
+    const bool act = ag + 32 * wr < nA && wc * NBW < nbt;
+    auto mfma = [&](int buf) {
+      if (!act) return;
+      bf16x8_t ah[2], al[2];
+#pragma unroll
+      for (int i = 0; i < 2; i++) {
+        const int row = buf * SAG + 32 * wr + 16 * i + c;
+        ah[i] = *(const bf16x8_t*)(Ahi + row * SKP + 8 * g);
+        al[i] = *(const bf16x8_t*)(Alo + row * SKP + 8 * g);
       }
-      __syncthreads();
-      // 32 features per MFMA; per B tile the products accumulate in feature
-      // order, hi.hi' then hi.lo' then lo.hi' within each 32
 #pragma unroll
-      for (int kk = 0; kk < SKC / 32; kk++) {
-        const bf16x8_t ah = *(const bf16x8_t*)(Ahi + (wave * 16 + c) * SKP + 32 * kk + 8 * g);
-        const bf16x8_t al = *(const bf16x8_t*)(Alo + (wave * 16 + c) * SKP + 32 * kk + 8 * g);
+      for (int t0 = 0; t0 < NBW; t0 += BG) {
+        bf16x8_t bh[BG], bl[BG];
 #pragma unroll
-        for (int t = 0; t < NBT; t++) {
-          if (t < nbt) {
-            const bf16x8_t bh = *(const bf16x8_t*)(Bhi + (t * 16 + c) * SKP + 32 * kk + 8 * g);
-            const bf16x8_t bl = *(const bf16x8_t*)(Blo + (t * 16 + c) * SKP + 32 * kk + 8 * g);
-            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, acc[t], 0, 0, 0);
-            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, acc[t], 0, 0, 0);
-            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, acc[t], 0, 0, 0);
-          }
+        for (int j = 0; j < BG; j++) {
+          const int row = buf * BMAX + (wc * NBW + t0 + j) * 16 + c;
+          bh[j] = *(const bf16x8_t*)(Bhi + row * SKP + 8 * g);
+          bl[j] = *(const bf16x8_t*)(Blo + row * SKP + 8 * g);
         }
+#pragma unroll
+        for (int j = 0; j < BG; j++)
+#pragma unroll
+          for (int i = 0; i < 2; i++)
+            acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[j], ah[i], acc[i][t0 + j], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < BG; j++)
+#pragma unroll
+          for (int i = 0; i < 2; i++)
+            acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl[j], ah[i], acc[i][t0 + j], 0, 0, 0);
+#pragma unroll
+        for (int j = 0; j < BG; j++)
+#pragma unroll
+          for (int i = 0; i < 2; i++)
+            acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[j], al[i], acc[i][t0 + j], 0, 0, 0);
       }
+    };
+    // chunk kc: MFMAs on buffer kc & 1; chunk kc + 1 (in registers `nx`)
+    // staged into the other buffer; chunk kc + 3 loaded into `nx`
+    float4 r0[SPT], r1[SPT];
+    auto step = [&](int kc, float4(&nx)[SPT]) {
+      mfma(kc & 1);
+      if (kc + 1 < nck) stage(nx, (kc + 1) & 1);
+      if (kc + 3 < nck) load(nx, kc + 3);
+      __syncthreads();
+    };
+    load(r0, 0);
+    if (nck > 1) load(r1, 1);
+    stage(r0, 0);
+    if (nck > 2) load(r0, 2);
+    __syncthreads();
+    for (int kc = 0; kc < nck; kc += 2) {
+      step(kc, r1);
+      if (kc + 1 < nck) step(kc + 1, r0);
     }
-    // row norms: the SKC/4 threads of a row are adjacent lanes
+    // reciprocal row norms: the Q threads of a row are adjacent lanes
 #pragma unroll
     for (int w = 0; w < SPT; w++) {
       float v = ss[w];
 #pragma unroll
-      for (int o = 1; o < SKC / 4; o <<= 1) v += __shfl_xor(v, o, 64);
+      for (int o = 1; o < Q; o <<= 1) v += __shfl_xor(v, o, 64);
       const int u = tid + w * AD_NT;
-      const int r = u / (SKC / 4);
-      if (srow[w] && (u % (SKC / 4)) == 0) {
-        const int slot = r < SAG ? 2 * (ag + r) : 2 * (r - SAG) + 1;  // patch slot
-        nrm[slot] = fmaxf(sqrtf(v), 1e-12f);
-      }
+      if (sval[w] && (u % Q) == 0) rn[u / Q] = 1.0f / fmaxf(sqrtf(v), 1e-12f);
     }
     __syncthreads();
-    // cosine = dot / (n_a n_b); argmax over B, ties to the lowest B index
+    // best B per A over this wave's tiles; rows and columns past nA / nB
+    // read clamped or stale norms and are masked
 #pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const int aa = ag + wave * 16 + 4 * g + j;
-      const float na = aa < nA ? nrm[2 * aa] : 1.f;
+    for (int i = 0; i < 2; i++) {
+      const int ar = 32 * wr + 16 * i + c;  // A row within the pass
+      const float ra = rn[min(ar, max(nA - ag, 1) - 1)];
       float bv = -INFINITY;
       int bi = 0x7fffffff;
 #pragma unroll
-      for (int t = 0; t < NBT; t++) {
-        const int bb = t * 16 + c;
-        if (t < nbt && bb < nB) {
-          const float v = acc[t][j] / (na * nrm[2 * bb + 1]);
-          if (v > bv) {
-            bv = v;
-            bi = bb;
-          }
-        }
-      }
+      for (int t = 0; t < NBW; t++) {
+        const int b0 = (wc * NBW + t) * 16 + 4 * g;
+        const float4 rb = *(const float4*)(rn + SAG + b0);
+        const float rbj[4] = {rb.x, rb.y, rb.z, rb.w};
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1) {
-        const float ov = __shfl_xor(bv, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (ov > bv || (ov == bv && oi < bi)) {
-          bv = ov;
-          bi = oi;
+        for (int j = 0; j < 4; j++) {
+          const float v = (acc[i][t][j] * ra) * rbj[j];
+          const bool take = act && b0 + j < nB && v > bv;
+          bv = take ? v : bv;
+          bi = take ? b0 + j : bi;
         }
       }
-      if (c == 0 && aa < nA) {
-        bestsim[aa] = bv;
-        best[aa] = bi < nB ? bi : 0;  // bi >= nB only with non-finite x
+      // combine the 4 lanes of the token (lanes c, c + 16, c + 32, c + 48):
+      // each swap yields the lane's own pair and its partner's
+      {
+        const auto v16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(bv), __float_as_uint(bv), false, false);
+        const auto i16 = __builtin_amdgcn_permlane16_swap((unsigned)bi, (unsigned)bi, false, false);
+        const float v0 = __uint_as_float(v16[0]), v1 = __uint_as_float(v16[1]);
+        const int i0 = (int)i16[0], i1 = (int)i16[1];
+        const bool t1 = v1 > v0 || (v1 == v0 && i1 < i0);
+        bv = t1 ? v1 : v0;
+        bi = t1 ? i1 : i0;
       }
+      {
+        const auto v32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(bv), __float_as_uint(bv), false, false);
+        const auto i32 = __builtin_amdgcn_permlane32_swap((unsigned)bi, (unsigned)bi, false, false);
+        const float v0 = __uint_as_float(v32[0]), v1 = __uint_as_float(v32[1]);
+        const int i0 = (int)i32[0], i1 = (int)i32[1];
+        const bool t1 = v1 > v0 || (v1 == v0 && i1 < i0);
+        bv = t1 ? v1 : v0;
+        bi = t1 ? i1 : i0;
+      }
+      if (g == 0) {
+        pbv[wc * SAG + ar] = bv;
+        pbi[wc * SAG + ar] = bi;
+      }
+    }
+    __syncthreads();
+    // partial results in B order: a later group wins only on a larger value
+    for (int e = tid; e < SAG && ag + e < nA; e += AD_NT) {
+      float v0 = pbv[e];
+      int i0 = pbi[e];
+#pragma unroll
+      for (int w = 1; w < WC; w++) {
+        const float v1 = pbv[w * SAG + e];
+        const int i1 = pbi[w * SAG + e];
+        if (v1 > v0 || (v1 == v0 && i1 < i0)) {
+          v0 = v1;
+          i0 = i1;
+        }
+      }
+      bestsim[ag + e] = v0;
+      best[ag + e] = i0 < nB ? i0 : 0;  // i0 >= nB only with non-finite x
     }
     __syncthreads();
   }
@@ -261,23 +348,28 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   const int d = a.d;
   const size_t tr_row = (size_t)(a.b - 1) * a.B + orig;
 
-  constexpr int TMAX = Z::TMAX, AMAX = Z::AMAX, BMAX = Z::BMAX, SKP = Z::SKP;
+  constexpr int TMAX = Z::TMAX, AMAX = Z::AMAX, BMAX = Z::BMAX, SKP = Z::SKP, SAG = Z::SAG;
   __shared__ float sc[TMAX];
   __shared__ float szs[TMAX];
   __shared__ int keepf[TMAX];
-  __shared__ float nrm[TMAX];
+  __shared__ int knew[TMAX];
+  __shared__ __attribute__((aligned(16))) float rn[TMAX];  // reciprocal norms
   __shared__ float bestsim[AMAX];
   __shared__ int best[AMAX];
   __shared__ int chosen[AMAX];
   __shared__ int clist[AMAX];
   __shared__ int cdst[AMAX];
   __shared__ int glead[AMAX];
+  __shared__ int srt[AMAX];
   __shared__ float tmpf[AMAX];
   __shared__ float tmps[AMAX];
-  __shared__ __attribute__((aligned(16))) bf16_t Ahi[SAG * SKP];
-  __shared__ __attribute__((aligned(16))) bf16_t Alo[SAG * SKP];
-  __shared__ __attribute__((aligned(16))) bf16_t Bhi[BMAX * SKP];
-  __shared__ __attribute__((aligned(16))) bf16_t Blo[BMAX * SKP];
+  // similarity operands, two buffers each
+  __shared__ __attribute__((aligned(16))) bf16_t Ahi[2 * SAG * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Alo[2 * SAG * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bhi[2 * BMAX * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Blo[2 * BMAX * SKP];
+  __shared__ float pbv[Z::WC * SAG];
+  __shared__ int pbi[Z::WC * SAG];
   __shared__ float red[16];
   __shared__ int ired[16];
 
@@ -312,46 +404,74 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   }
   const int nA = (N + 1) / 2, nB = N / 2;
   if (r > 0) {
-    similarity_argmax<Z>(a.x, base, d, nA, nB, nrm, bestsim, best, Ahi, Alo, Bhi, Blo);
-    // top-r of A by best similarity, ties to the lower A slot
-    for (int aa = tid; aa < nA; aa += AD_NT) {
-      const float v = bestsim[aa];
-      int rank = 0;
-      for (int a2 = 0; a2 < nA; a2++) {
-        const float v2 = bestsim[a2];
-        rank += (v2 > v) || (v2 == v && a2 < aa);
+    similarity_argmax<Z>(a.x, base, d, nA, nB, rn, bestsim, best, Ahi, Alo, Bhi, Blo, pbv,
+                         pbi);
+    // top-r of A by best similarity, ties to the lower A slot; P adjacent
+    // lanes split the comparisons of one element
+    {
+      const int P = rank_lanes(nA), p = tid % P;
+      for (int e0 = 0; e0 < nA; e0 += AD_NT / P) {
+        const int aa = e0 + tid / P;
+        int rank = 0;
+        if (aa < nA) {
+          const float v = bestsim[aa];
+          for (int a2 = p; a2 < nA; a2 += P) {
+            const float v2 = bestsim[a2];
+            rank += (v2 > v) || (v2 == v && a2 < aa);
+          }
+        }
+        for (int o = 1; o < P; o <<= 1) rank += __shfl_xor(rank, o, 64);
+        if (aa < nA && p == 0) chosen[aa] = rank < r;
       }
-      chosen[aa] = rank < r;
     }
     __syncthreads();
     // chosen sources in ascending A slot: clist[0 .. r)
     block_compact(tid < nA && chosen[tid], tid, clist, ired);
-    // destination of each; a source leads its group when no earlier chosen
-    // source has the same destination.  Groups are merged independently,
-    // each summing its sources in ascending A slot.
+    // destination of each, and the sources sorted by (destination, A slot):
+    // srt[0 .. r) lists the positions q in clist; the sources of one
+    // destination form a group, contiguous in srt and in ascending A slot.
+    // Groups are merged independently.
     for (int q = tid; q < r; q += AD_NT) cdst[q] = best[clist[q]];
     __syncthreads();
-    bool lead = false;
-    if (tid < r) {
-      const int bb = cdst[tid];
-      lead = true;
-      for (int q2 = 0; q2 < tid; q2++) lead = lead && (cdst[q2] != bb);
+    {
+      const int P = rank_lanes(r), p = tid % P;
+      for (int e0 = 0; e0 < r; e0 += AD_NT / P) {
+        const int q = e0 + tid / P;
+        int rank = 0;
+        if (q < r) {
+          const int key = cdst[q];
+          for (int q2 = p; q2 < r; q2 += P) {
+            const int k2 = cdst[q2];
+            rank += (k2 < key) || (k2 == key && q2 < q);
+          }
+        }
+        for (int o = 1; o < P; o <<= 1) rank += __shfl_xor(rank, o, 64);
+        if (q < r && p == 0) srt[rank] = q;
+      }
     }
-    const int ng = block_compact(lead, tid, glead, ired);
-    // size-weighted merge into each receiving destination (16-byte pieces)
+    __syncthreads();
+    const bool start = tid < r && (tid == 0 || cdst[srt[tid]] != cdst[srt[tid - 1]]);
+    const int ng = block_compact(start, tid, glead, ired);  // glead[k]: first position of group k
+    // size-weighted merge into each receiving destination (16-byte pieces);
+    // the destination row and the group's first source are loaded together
     const int d4 = d / 4;
     float4* x4 = (float4*)a.x;
     for (int idx = tid; idx < ng * d4; idx += AD_NT) {
       const int k = idx / d4, f = idx - k * d4;
-      const int q0 = glead[k], bb = cdst[q0];
+      const int p0 = glead[k], p1 = k + 1 < ng ? glead[k + 1] : r;
+      const int bb = cdst[srt[p0]], a0 = clist[srt[p0]];
       const size_t rowb = (size_t)(base + 2 + 2 * bb);
-      const float sb = szs[2 + 2 * bb];
       const float4 xb = x4[rowb * d4 + f];
+      const float4 xa0 = x4[(size_t)(base + 1 + 2 * a0) * d4 + f];
+      const float sb = szs[2 + 2 * bb], sa0 = szs[1 + 2 * a0];
       float4 num = make_float4(sb * xb.x, sb * xb.y, sb * xb.z, sb * xb.w);
-      float den = sb;
-      for (int q = q0; q < r; q++) {
-        if (cdst[q] != bb) continue;
-        const int aa = clist[q];
+      num.x = num.x + sa0 * xa0.x;
+      num.y = num.y + sa0 * xa0.y;
+      num.z = num.z + sa0 * xa0.z;
+      num.w = num.w + sa0 * xa0.w;
+      float den = sb + sa0;
+      for (int pp = p0 + 1; pp < p1; pp++) {
+        const int aa = clist[srt[pp]];
         const float sa = szs[1 + 2 * aa];
         const float4 xa = x4[(size_t)(base + 1 + 2 * aa) * d4 + f];
         num.x = num.x + sa * xa.x;
@@ -363,20 +483,21 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
       x4[rowb * d4 + f] = make_float4(num.x / den, num.y / den, num.z / den, num.w / den);
     }
     for (int k = tid; k < ng; k += AD_NT) {
-      const int q0 = glead[k], bb = cdst[q0];
+      const int p0 = glead[k], p1 = k + 1 < ng ? glead[k + 1] : r;
+      const int bb = cdst[srt[p0]];
       float den = szs[2 + 2 * bb];
       float s2 = attnP ? sc[2 + 2 * bb] : 0.f;
-      for (int q = q0; q < r; q++) {
-        if (cdst[q] != bb) continue;
-        den = den + szs[1 + 2 * clist[q]];
-        if (attnP) s2 = s2 + sc[1 + 2 * clist[q]];
+      for (int pp = p0; pp < p1; pp++) {
+        const int aa = clist[srt[pp]];
+        den = den + szs[1 + 2 * aa];
+        if (attnP) s2 = s2 + sc[1 + 2 * aa];
       }
       tmpf[k] = den;
       tmps[k] = s2;
     }
     __syncthreads();
     for (int k = tid; k < ng; k += AD_NT) {
-      const int bb = cdst[glead[k]];
+      const int bb = cdst[srt[glead[k]]];
       a.size[base + 2 + 2 * bb] = tmpf[k];
       if (attnP) sc[2 + 2 * bb] = tmps[k];
     }
@@ -438,26 +559,27 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     for (int t = 1 + tid; t < T; t += AD_NT) ns += keepf[t];
     ns = bsum_i(ns, ired);
     const int k = (int)floor(__dmul_rn(a.tau_eff, (double)ns));
-    constexpr int U = (TMAX + AD_NT - 1) / AD_NT;
-    int keep_new[U];
-#pragma unroll
-    for (int u = 0; u < U; u++) {
-      const int t = 1 + tid + u * AD_NT;
-      keep_new[u] = 0;
-      if (t < T && keepf[t]) {
-        const float v = sc[t];
+    // rank among the kept patch tokens by score, ties to the lower slot;
+    // P adjacent lanes split the comparisons of one token
+    {
+      const int P = rank_lanes(T - 1), p = tid % P;
+      for (int e0 = 0; e0 < T - 1; e0 += AD_NT / P) {
+        const int t = 1 + e0 + tid / P;
+        const bool act = t < T && keepf[t];
         int rank = 0;
-        for (int t2 = 1; t2 < T; t2++)
-          if (keepf[t2]) rank += (sc[t2] > v) || (sc[t2] == v && t2 < t);
-        keep_new[u] = rank < k;
+        if (act) {
+          const float v = sc[t];
+          for (int t2 = 1 + p; t2 < T; t2 += P) {
+            const float v2 = sc[t2];
+            rank += keepf[t2] & ((v2 > v) | (v2 == v && t2 < t));
+          }
+        }
+        for (int o = 1; o < P; o <<= 1) rank += __shfl_xor(rank, o, 64);
+        if (t < T && p == 0) knew[t] = act && rank < k;
       }
     }
     __syncthreads();
-#pragma unroll
-    for (int u = 0; u < U; u++) {
-      const int t = 1 + tid + u * AD_NT;
-      if (t < T) keepf[t] = keep_new[u];
-    }
+    for (int t = 1 + tid; t < T; t += AD_NT) keepf[t] = knew[t];
     __syncthreads();
   }
 
