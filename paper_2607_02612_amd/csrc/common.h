@@ -106,11 +106,21 @@ __device__ __forceinline__ int block_sum256_i(int v, int* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// Sum over the 32 lanes of a half wave (lanes 0-31 or 32-63).
+// Sum over the 32 lanes of a half wave (lanes 0-31 or 32-63) without LDS
+// round trips: DPP swaps within quads (lane ^ 1, lane ^ 2), the mirrors of
+// 8- and 16-lane rows, then the row swap of permlane16.  After each step the
+// partners hold the same two summands in opposite order, so all 32 lanes end
+// with the same bits.
+template <int CTRL>
+__device__ __forceinline__ float dpp_peer(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
 __device__ __forceinline__ float half_sum(float v) {
-#pragma unroll
-  for (int o = 16; o > 0; o >>= 1) v += __shfl_xor(v, o, 32);
-  return v;
+  v += dpp_peer<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_peer<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_peer<0x141>(v);  // row_half_mirror
+  v += dpp_peer<0x140>(v);  // row_mirror
+  return sum_xor16(v);
 }
 
 // Four floats -> storage type, one vector store.
