@@ -189,21 +189,29 @@ __device__ __forceinline__ void ln_row_half(const float* __restrict__ xr, int d,
 
 // GELU with the exact (erf) form, v Phi(v), Phi the standard normal CDF,
 // written as GELU(v) = max(v, 0) - |v| Q(|v|) with the upper tail
-// Q(a) = erfc(a / sqrt 2) / 2 from the rational approximation 7.1.26 of
+// Q(a) = erfc(a / sqrt 2) / 2 from the rational approximation 7.1.28 of
 // Abramowitz & Stegun (Handbook of Mathematical Functions):
-//   erfc(z) = t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-z^2),
-//   t = 1 / (1 + p z), |error| <= 1.5e-7,
-// with z = a / sqrt 2 folded into p and into the exponent and the 1/2 into
-// a1..a5.  The tail form has no cancellation for negative v.
+//   erfc(z) = (1 + a1 z + a2 z^2 + a3 z^3 + a4 z^4 + a5 z^5 + a6 z^6)^-16,
+//   |error| <= 3e-7,
+// one reciprocal and four squarings.  z = a / sqrt 2 is folded into the
+// coefficients, and the 1/2 through a common factor 2^(1/16) on all of them
+// (P^-16 scales by 1/2).  The tail form has no cancellation for negative v;
+// past |v| of about 11 the power underflows and the result is max(v, 0).
 __device__ __forceinline__ float gelu_erf(float v) {
   const float a = fabsf(v);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.70710678118654752f, a, 1.0f));
-  float y = fmaf(t, 0.5f * 1.061405429f, 0.5f * -1.453152027f);
-  y = fmaf(t, y, 0.5f * 1.421413741f);
-  y = fmaf(t, y, 0.5f * -0.284496736f);
-  y = fmaf(t, y, 0.5f * 0.254829592f);
-  const float e = __builtin_amdgcn_exp2f(v * (v * (-0.5f * 1.4426950408889634f)));
-  return fmaf(-a, (t * y) * e, fmaxf(v, 0.f));
+  // 2^(1/16) a_k 2^(-k/2), k = 6 .. 0 (a_0 = 1)
+  float p = fmaf(a, 5.621299664e-06f, 5.105520901e-05f);
+  p = fmaf(a, p, 3.968613701e-05f);
+  p = fmaf(a, p, 3.422739239e-03f);
+  p = fmaf(a, p, 2.207699846e-02f);
+  p = fmaf(a, p, 5.207516304e-02f);
+  p = fmaf(a, p, 1.044273782e+00f);
+  float r = __builtin_amdgcn_rcpf(p);
+  r = r * r;
+  r = r * r;
+  r = r * r;
+  r = r * r;
+  return fmaf(-a, r, fmaxf(v, 0.f));
 }
 
 }  // namespace fusion
