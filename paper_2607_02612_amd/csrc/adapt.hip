@@ -4,6 +4,9 @@
 //   (Eq. 6-7), CLS-attention top-k pruning of continuing samples (Eq. 8),
 // followed by a separate compaction kernel that re-packs the surviving
 // samples and tokens (exclusive scans over new lengths and keep flags).
+// The fp32 rows of x never move: a token keeps its physical row (a merge
+// updates the destination row in place) and the compaction re-packs the row
+// map, the sizes and the origin ids.
 //
 // One 512-thread workgroup per live sample (the compaction uses 256).  No
 // float atomics: every reduction has a fixed order, so results do not depend
@@ -142,7 +145,7 @@ __device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
 // LDS (pbv, pbi: WC SAG entries each).  rn holds the reciprocal norms:
 // A rows of the pass at [0, SAG), B rows at [SAG, SAG + BMAX).
 template <class Z>
-__device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
+__device__ void similarity_argmax(const float* __restrict__ x, const int* prow, int d,
                                   int nA, int nB, float* rn, float* bestsim,
                                   int* best, bf16_t* Ahi, bf16_t* Alo,
                                   bf16_t* Bhi, bf16_t* Blo, float* pbv, int* pbi) {
@@ -157,8 +160,8 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
   const int wr = wave / WC, wc = wave % WC;
   const int nbt = (nB + 15) >> 4, nck = d / SKC;
   for (int ag = 0; ag < nA; ag += SAG) {
-    const float* xs = x + (size_t)base * d;
-    int soff[SPT];  // slot offsets from the sample's first row, in floats
+    const float* xs = x;
+    uint32_t soff[SPT];  // slot offsets into x, in floats (physical row * d + feature)
     bool sval[SPT];
     float ss[SPT];
 #pragma unroll
@@ -167,10 +170,10 @@ __device__ void similarity_argmax(const float* __restrict__ x, int base, int d,
       const int r = u / Q, q = (u % Q) * 4;
       if (r < SAG) {
         sval[w] = ag + r < nA;
-        soff[w] = (1 + 2 * min(ag + r, nA - 1)) * d + q;
+        soff[w] = (uint32_t)prow[1 + 2 * min(ag + r, nA - 1)] * d + q;
       } else {
         sval[w] = r - SAG < nB;
-        soff[w] = (2 + 2 * min(r - SAG, nB - 1)) * d + q;
+        soff[w] = (uint32_t)prow[2 + 2 * min(r - SAG, nB - 1)] * d + q;
       }
       ss[w] = 0.f;
     }
@@ -351,6 +354,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   constexpr int TMAX = Z::TMAX, AMAX = Z::AMAX, BMAX = Z::BMAX, SKP = Z::SKP, SAG = Z::SAG;
   __shared__ float sc[TMAX];
   __shared__ float szs[TMAX];
+  __shared__ int prow[TMAX];  // physical row of x for each of the sample's tokens
   __shared__ int keepf[TMAX];
   __shared__ int knew[TMAX];
   __shared__ __attribute__((aligned(16))) float rn[TMAX];  // reciprocal norms
@@ -379,6 +383,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   for (int t = tid; t < T; t += AD_NT) {
     keepf[t] = 1;
     szs[t] = a.size[base + t];
+    prow[t] = a.rmap[base + t];
   }
   if (attnP) {
     for (int t = tid; t < T; t += AD_NT) {
@@ -393,7 +398,8 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   int r = 0;
   if (a.isM) {
     float z = 0.f;
-    for (int k = tid; k < d; k += AD_NT) z = fmaf(a.router_w[k], a.x[(size_t)base * d + k], z);
+    const float* xc = a.x + (size_t)prow[0] * d;
+    for (int k = tid; k < d; k += AD_NT) z = fmaf(a.router_w[k], xc[k], z);
     z = bsum(z, red) + a.router_b[0];
     const float m = 1.0f / (1.0f + expf(-z));
     r = merge_count(m, a.rho, a.r_b, N, a.merge_rule);
@@ -404,7 +410,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   }
   const int nA = (N + 1) / 2, nB = N / 2;
   if (r > 0) {
-    similarity_argmax<Z>(a.x, base, d, nA, nB, rn, bestsim, best, Ahi, Alo, Bhi, Blo, pbv,
+    similarity_argmax<Z>(a.x, prow, d, nA, nB, rn, bestsim, best, Ahi, Alo, Bhi, Blo, pbv,
                          pbi);
     // top-r of A by best similarity, ties to the lower A slot; P adjacent
     // lanes split the comparisons of one element
@@ -460,9 +466,9 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
       const int k = idx / d4, f = idx - k * d4;
       const int p0 = glead[k], p1 = k + 1 < ng ? glead[k + 1] : r;
       const int bb = cdst[srt[p0]], a0 = clist[srt[p0]];
-      const size_t rowb = (size_t)(base + 2 + 2 * bb);
+      const size_t rowb = (size_t)prow[2 + 2 * bb];
       const float4 xb = x4[rowb * d4 + f];
-      const float4 xa0 = x4[(size_t)(base + 1 + 2 * a0) * d4 + f];
+      const float4 xa0 = x4[(size_t)prow[1 + 2 * a0] * d4 + f];
       const float sb = szs[2 + 2 * bb], sa0 = szs[1 + 2 * a0];
       float4 num = make_float4(sb * xb.x, sb * xb.y, sb * xb.z, sb * xb.w);
       num.x = num.x + sa0 * xa0.x;
@@ -473,7 +479,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
       for (int pp = p0 + 1; pp < p1; pp++) {
         const int aa = clist[srt[pp]];
         const float sa = szs[1 + 2 * aa];
-        const float4 xa = x4[(size_t)(base + 1 + 2 * aa) * d4 + f];
+        const float4 xa = x4[(size_t)prow[1 + 2 * aa] * d4 + f];
         num.x = num.x + sa * xa.x;
         num.y = num.y + sa * xa.y;
         num.z = num.z + sa * xa.z;
@@ -540,7 +546,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     const float pb = a.prune_b[0];
     for (int t = 1 + hw; t < T; t += AD_NT / 32) {
       if (!keepf[t]) continue;
-      const float4* xr = (const float4*)(a.x + (size_t)(base + t) * d);
+      const float4* xr = (const float4*)(a.x + (size_t)prow[t] * d);
       float s = 0.f;
       for (int q = hl; q < d4; q += 32) {
         const float4 v = xr[q], w = w4[q];
@@ -676,20 +682,24 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   }
   __syncthreads();
   // kept rows of this part (the sample's rows split into CP_PARTS ranges):
-  // one half wave per row copies it (16-byte pieces) and, when asked,
-  // writes its LayerNorm for the next block
+  // when asked, one half wave per row writes its LayerNorm for the next
+  // block (16-byte pieces); the row itself stays where it is, only its
+  // physical row id, size and origin move to the packed slot
   const int per = (Tn + CP_PARTS - 1) / CP_PARTS;
   const int t0 = part * per, t1 = min(Tn, t0 + per);
-  for (int t = t0 + (tid >> 5); t < t1; t += 8) {
-    const int dj = dsts[t];
-    if (dj < 0) continue;
-    const size_t dr = (size_t)(off + dj);
-    ln_row_half<T>(a.x + (size_t)(base + t) * a.d, a.d, lane & 31, a.ln_g, a.ln_b,
-                   a.ln_out ? (T*)a.ln_out + dr * a.d : nullptr, a.x2 + dr * a.d);
+  if (a.ln_out) {
+    for (int t = t0 + (tid >> 5); t < t1; t += 8) {
+      const int dj = dsts[t];
+      if (dj < 0) continue;
+      const size_t dr = (size_t)(off + dj);
+      ln_row_half<T>(a.x + (size_t)a.rmap[base + t] * a.d, a.d, lane & 31, a.ln_g, a.ln_b,
+                     (T*)a.ln_out + dr * a.d, nullptr);
+    }
   }
   for (int t = t0 + tid; t < t1; t += 256) {
     const int dj = dsts[t];
     if (dj < 0) continue;
+    a.rmap2[off + dj] = a.rmap[base + t];
     a.size2[off + dj] = a.size[base + t];
     a.origin2[off + dj] = a.origin[base + t];
     if (a.tr_ids)

@@ -276,7 +276,8 @@ struct fusion_model {
   const void *pe_w, *head_w;
   BlockW blk[FUSION_MAX_LAYERS];
   // workspace
-  float* x[2];
+  float* x;        // [Mmax, d] fp32 residual stream; rows never move
+  int* rmap[2];    // packed row -> physical row of x (ping-pong)
   float* size[2];
   int* origin[2];
   int* cu[2];
@@ -377,13 +378,13 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
   int cur = 0;
   {
     Prof p(m, s, K_INIT);
-    HIP_OR_FAIL(launch_init(m->x[0], m->size[0], m->origin[0], m->cu[0], m->live[0],
+    HIP_OR_FAIL(launch_init(m->x, m->rmap[0], m->size[0], m->origin[0], m->cu[0], m->live[0],
                             m->cnt[0], token_counts, m->cls, m->pos, B, n0, d, L, s));
   }
   {
     Prof p(m, s, K_PATCH);
     HIP_OR_FAIL(launch_patchify<T>(images, (T*)m->ffn, B, c.in_ch, c.img, c.patch, s));
-    Epi e{EPI_PATCH, m->x[0], d, m->pe_b, nullptr, m->pos, n0};
+    Epi e{EPI_PATCH, m->x, d, m->pe_b, nullptr, m->pos, n0};
     HIP_OR_FAIL(launch_gemm<T>((const T*)m->ffn, c.pdim, (const T*)m->pe_w, d, c.pdim,
                                nullptr, B * n0, B * n0, e, s));
   }
@@ -404,7 +405,7 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
     const int* Mdev = &m->cnt[cur]->M;
     if (!ln1_done) {
       Prof p(m, s, K_LN);
-      HIP_OR_FAIL(launch_layernorm<T>(m->x[cur], w.ln1_g, w.ln1_b, (T*)m->act, d, m->cnt[cur],
+      HIP_OR_FAIL(launch_layernorm<T>(m->x, m->rmap[cur], w.ln1_g, w.ln1_b, (T*)m->act, d, m->cnt[cur],
                                       m->cu[cur], m->live[cur], 0, M_ub, nullptr, L, s));
     }
     ln1_done = false;
@@ -428,13 +429,13 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
     }
     {
       Prof p(m, s, K_PROJ);
-      Epi e{EPI_RESID, m->x[cur], d, w.proj_b, nullptr, nullptr, 0};
+      Epi e{EPI_RESID, m->x, d, w.proj_b, m->rmap[cur], nullptr, 0};
       HIP_OR_FAIL(launch_gemm<T>((const T*)m->act, d, (const T*)w.proj_w, d, d, Mdev, 0, M_ub, e, s));
     }
     if (o.stop_block == b && o.stop_stage == 1) break;
     {
       Prof p(m, s, K_LN);
-      HIP_OR_FAIL(launch_layernorm<T>(m->x[cur], w.ln2_g, w.ln2_b, (T*)m->act, d, m->cnt[cur],
+      HIP_OR_FAIL(launch_layernorm<T>(m->x, m->rmap[cur], w.ln2_g, w.ln2_b, (T*)m->act, d, m->cnt[cur],
                                       m->cu[cur], m->live[cur], 0, M_ub, nullptr, L, s));
     }
     {
@@ -444,7 +445,7 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
     }
     {
       Prof p(m, s, K_FC2);
-      Epi e{EPI_RESID, m->x[cur], d, w.fc2_b, nullptr, nullptr, 0};
+      Epi e{EPI_RESID, m->x, d, w.fc2_b, m->rmap[cur], nullptr, 0};
       HIP_OR_FAIL(launch_gemm<T>((const T*)m->ffn, c.mlp, (const T*)w.fc2_w, d, c.mlp, Mdev, 0,
                                  M_ub, e, s));
     }
@@ -457,10 +458,10 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
       const int kind = c.exit_kind[b - 1];
       const int* nl = &m->cnt[cur]->nlive;
       if (kind == FUSION_EXIT_POOL_MLP)
-        HIP_OR_FAIL(launch_pool_ln<T>(m->x[cur], m->size[cur], m->cu[cur], m->cnt[cur], w.eln_g,
+        HIP_OR_FAIL(launch_pool_ln<T>(m->x, m->rmap[cur], m->size[cur], m->cu[cur], m->cnt[cur], w.eln_g,
                                       w.eln_b, (T*)m->hc, d, B, s));
       else
-        HIP_OR_FAIL(launch_layernorm<T>(m->x[cur], w.eln_g, w.eln_b, (T*)m->hc, d, m->cnt[cur],
+        HIP_OR_FAIL(launch_layernorm<T>(m->x, m->rmap[cur], w.eln_g, w.eln_b, (T*)m->hc, d, m->cnt[cur],
                                         m->cu[cur], m->live[cur], 1, B, nullptr, L, s));
       if (kind == FUSION_EXIT_LINEAR) {
         Epi e{EPI_F32, m->head_buf, c.C, w.eb, nullptr, nullptr, 0};
@@ -481,8 +482,8 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
       {
         Prof p(m, s, K_ADAPT);
         AdaptArgs a{};
-        a.x = m->x[cur]; a.size = m->size[cur]; a.origin = m->origin[cur]; a.cu = m->cu[cur];
-        a.live = m->live[cur]; a.cnt = m->cnt[cur];
+        a.x = m->x; a.rmap = m->rmap[cur]; a.size = m->size[cur]; a.origin = m->origin[cur];
+        a.cu = m->cu[cur]; a.live = m->live[cur]; a.cnt = m->cnt[cur];
         a.d = d; a.H = c.heads; a.n0 = n0; a.C = c.C; a.L = L; a.B = B; a.b = b;
         a.isM = isM; a.isE = isE; a.isP = isP;
         a.merge_rule = c.merge_rule; a.prune_rule = c.prune_rule;
@@ -501,9 +502,10 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
         Prof p(m, s, K_COMPACT);
         const int nx = cur ^ 1;
         CompactArgs a{};
-        a.x = m->x[cur]; a.size = m->size[cur]; a.origin = m->origin[cur]; a.cu = m->cu[cur];
-        a.live = m->live[cur]; a.cnt = m->cnt[cur]; a.keep = m->keep; a.newlen = m->newlen;
-        a.x2 = m->x[nx]; a.size2 = m->size[nx]; a.origin2 = m->origin[nx]; a.cu2 = m->cu[nx];
+        a.x = m->x; a.rmap = m->rmap[cur]; a.size = m->size[cur]; a.origin = m->origin[cur];
+        a.cu = m->cu[cur]; a.live = m->live[cur]; a.cnt = m->cnt[cur]; a.keep = m->keep;
+        a.newlen = m->newlen;
+        a.rmap2 = m->rmap[nx]; a.size2 = m->size[nx]; a.origin2 = m->origin[nx]; a.cu2 = m->cu[nx];
         a.live2 = m->live[nx]; a.cnt2 = m->cnt[nx];
         a.d = d; a.n0 = n0; a.B = B; a.b = b; a.tr_ids = tr ? tr->ids : nullptr;
         a.nlive_ub = B;
@@ -527,7 +529,7 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
   if (o.stop_block > 0) return FUSION_OK;
   {
     Prof p(m, s, K_FINAL_HEAD);
-    HIP_OR_FAIL(launch_layernorm<T>(m->x[cur], m->norm_g, m->norm_b, (T*)m->hc, d, m->cnt[cur],
+    HIP_OR_FAIL(launch_layernorm<T>(m->x, m->rmap[cur], m->norm_g, m->norm_b, (T*)m->hc, d, m->cnt[cur],
                                     m->cu[cur], m->live[cur], 1, B, exit_block, L, s));
     Epi e{EPI_F32, logits, c.C, m->head_b, m->live[cur], nullptr, 0};
     HIP_OR_FAIL(launch_gemm<T>((const T*)m->hc, d, (const T*)m->head_w, c.C, d,
@@ -666,8 +668,13 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
   const size_t esz = c.precision == 1 ? 2 : 4;
   const size_t Mmax = (size_t)max_batch * (c.n0 + 1);
   const size_t ffn_cols = std::max<size_t>(c.mlp, c.pdim);
+  // x offsets are 32-bit in the adapt kernel's similarity loads
+  if (Mmax * (size_t)c.d > (size_t)INT32_MAX)
+    return bail(fail(FUSION_E_CAPACITY,
+                     "max_batch too large: the residual stream would exceed 2^31 elements"));
+  m->x = (float*)dev_alloc<float>(m, Mmax * c.d * 4, &rc);
   for (int k = 0; k < 2; k++) {
-    m->x[k] = (float*)dev_alloc<float>(m, Mmax * c.d * 4, &rc);
+    m->rmap[k] = (int*)dev_alloc<int>(m, Mmax * 4, &rc);
     m->size[k] = (float*)dev_alloc<float>(m, Mmax * 4, &rc);
     m->origin[k] = (int*)dev_alloc<int>(m, Mmax * 4, &rc);
     m->cu[k] = (int*)dev_alloc<int>(m, (max_batch + 1) * 4, &rc);
@@ -763,7 +770,7 @@ FUSION_API int fusion_debug_state(fusion_model* m, const float* images, int batc
   int cur = 0;
   int rc = run_common(m, images, batch, lg, eb, tc, o, stream, &cur);
   if (rc == FUSION_OK) {
-    hipError_t e = launch_copy_state(m->x[cur], m->cu[cur], m->live[cur], m->cnt[cur], x_out,
+    hipError_t e = launch_copy_state(m->x, m->rmap[cur], m->cu[cur], m->live[cur], m->cnt[cur], x_out,
                                      cu_out, live_out, m->cfg.d, batch * (m->cfg.n0 + 1), batch, s);
     LiveCounts hc{};
     if (e == hipSuccess) e = hipMemcpyAsync(&hc, m->cnt[cur], sizeof(hc), hipMemcpyDeviceToHost, s);

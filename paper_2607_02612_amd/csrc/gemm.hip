@@ -23,7 +23,7 @@ __device__ __forceinline__ void epilogue(const Epi& e, int r, int n, float acc) 
       ((T*)e.out)[(size_t)r * e.ldo + n] = St<T>::put(gelu_erf(acc + e.bias[n]));
       break;
     case EPI_RESID: {
-      float* p = (float*)e.out + (size_t)r * e.ldo + n;
+      float* p = (float*)e.out + (size_t)(e.rows ? e.rows[r] : r) * e.ldo + n;
       *p = *p + (acc + e.bias[n]);
       break;
     }
@@ -338,14 +338,22 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
       // the addend: the residual row (x += ...) or, for the patch
       // embedding, the position embedding of patch token 1 + j, whose
       // output row is s (n0 + 1) + 1 + j for packed row r = s n0 + j
+      // (residual rows through the row map, whose entries are fetched first)
       float4 xv[PER];
+      int prow[PER];
+#pragma unroll
+      for (int k = 0; k < PER; k++) {
+        const int idx = tid + k * NT;
+        const int m = min(m0 + rb + idx / (NB / 4), M - 1);
+        prow[k] = (EPI == EPI_RESID && e.rows) ? e.rows[m] : m;
+      }
 #pragma unroll
       for (int k = 0; k < PER; k++) {
         const int idx = tid + k * NT;
         const int r = idx / (NB / 4), ch = idx % (NB / 4);
         const int m = min(m0 + rb + r, M - 1), n = min(n0 + ch * 4, N - 4);
         if (EPI == EPI_RESID) {
-          xv[k] = *(const float4*)(x + (size_t)m * e.ldo + n);
+          xv[k] = *(const float4*)(x + (size_t)prow[k] * e.ldo + n);
         } else {
           const int pj = m - (m / e.n0) * e.n0;
           xv[k] = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + n);
@@ -358,7 +366,7 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
         const int m = m0 + rb + r, n = n0 + ch * 4;
         const float4 sv = *(const float4*)(smem + r * (NB * 4) + ((ch ^ (r & 31)) << 4));
         if (m < M && n < N) {
-          size_t orow = (size_t)m;
+          size_t orow = (size_t)prow[k];
           if (EPI == EPI_PATCH) {
             const int sidx = m / e.n0;
             orow = (size_t)sidx * (e.n0 + 1) + 1 + (m - sidx * e.n0);
@@ -378,7 +386,7 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
     if (m >= M) continue;
     size_t orow = (size_t)m;
     int pj = 0;
-    if (EPI == EPI_F32) orow = e.rows ? (size_t)e.rows[m] : (size_t)m;
+    if (EPI == EPI_F32 || EPI == EPI_RESID) orow = e.rows ? (size_t)e.rows[m] : (size_t)m;
     if (EPI == EPI_PATCH) {
       const int sidx = m / e.n0;
       pj = m - sidx * e.n0;

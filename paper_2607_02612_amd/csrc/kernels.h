@@ -11,7 +11,7 @@ namespace fusion {
 enum EpiMode {
   EPI_STORE = 0,  // out(T)[r, n]  = acc + bias[n]
   EPI_GELU = 1,   // out(T)[r, n]  = GELU(acc + bias[n])
-  EPI_RESID = 2,  // x(f32)[r, n]  = x[r, n] + (acc + bias[n])
+  EPI_RESID = 2,  // x(f32)[p, n] = x[p, n] + (acc + bias[n]), p = rows ? rows[r] : r
   EPI_F32 = 3,    // out(f32)[rows ? rows[r] : r, n] = acc + bias[n]
   EPI_PATCH = 4   // x(f32)[s (n0+1) + 1 + j, n] = (acc + bias[n]) + pos[1 + j, n],
                   //   r = s n0 + j
@@ -22,7 +22,7 @@ struct Epi {
   void* out;
   int ldo;
   const float* bias;
-  const int* rows;  // EPI_F32 scatter map (optional)
+  const int* rows;  // EPI_F32 scatter map / EPI_RESID row map of x (optional)
   const float* pos; // EPI_PATCH
   int n0;           // EPI_PATCH
 };
@@ -37,18 +37,24 @@ template <typename T>
 hipError_t launch_patchify(const float* img, T* out, int B, int C, int S,
                            int p, hipStream_t s);
 
-// State at the start of a run: unit sizes, origin ids, cu/live maps, CLS
-// rows of x, zeroed token counts.
-hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
+// The fp32 residual stream x keeps every token in the physical row it was
+// created in (merged tokens are updated in place); packed row r of the
+// current state lives in physical row rmap[r].  Compaction repacks rmap,
+// size and origin, not x.
+//
+// State at the start of a run: unit sizes, origin ids, identity row map,
+// cu/live maps, CLS rows of x, zeroed token counts.
+hipError_t launch_init(float* x, int* rmap, float* size, int* origin, int* cu, int* live,
                        LiveCounts* cnt, int* token_counts, const float* cls,
                        const float* pos, int B, int n0, int d, int L,
                        hipStream_t s);
 
-// LayerNorm of packed rows (cls_only = 0: rows 0..M-1 -> out rows 0..M-1;
-// cls_only = 1: row cu[i] of live sample i -> out row i).  When exit_block is
+// LayerNorm of packed rows, read through the row map (cls_only = 0: rows
+// 0..M-1 -> out rows 0..M-1; cls_only = 1: row cu[i] of live sample i -> out
+// row i).  When exit_block is
 // non-null (final head), also writes exit_block[live[i]] = L.
 template <typename T>
-hipError_t launch_layernorm(const float* x, const float* g, const float* b,
+hipError_t launch_layernorm(const float* x, const int* rmap, const float* g, const float* b,
                             T* out, int d, const LiveCounts* cnt,
                             const int* cu, const int* live, int cls_only,
                             int rows_ub, int* exit_block, int L, hipStream_t s);
@@ -56,7 +62,7 @@ hipError_t launch_layernorm(const float* x, const float* g, const float* b,
 // LayerNorm of the size-weighted mean of each live sample's patch rows
 // (pooled exit heads): out[i] = LN(sum_t s_t x_t / sum_t s_t).
 template <typename T>
-hipError_t launch_pool_ln(const float* x, const float* size, const int* cu,
+hipError_t launch_pool_ln(const float* x, const int* rmap, const float* size, const int* cu,
                           const LiveCounts* cnt, const float* g, const float* b,
                           T* out, int d, int nlive_ub, hipStream_t s);
 
@@ -81,6 +87,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
 struct AdaptArgs {
   float* x;
+  const int* rmap;  // packed row -> physical row of x
   float* size;
   const int* origin;
   const int* cu;
@@ -116,6 +123,7 @@ hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s);
 
 struct CompactArgs {
   const float* x;
+  const int* rmap;  // packed row -> physical row of x
   const float* size;
   const int* origin;
   const int* cu;
@@ -123,7 +131,7 @@ struct CompactArgs {
   const LiveCounts* cnt;
   const int* keep;
   const int* newlen;
-  float* x2;
+  int* rmap2;
   float* size2;
   int* origin2;
   int* cu2;
@@ -142,7 +150,7 @@ template <typename T>
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
 
 // Copy of the packed state for diagnostics.
-hipError_t launch_copy_state(const float* x, const int* cu, const int* live,
+hipError_t launch_copy_state(const float* x, const int* rmap, const int* cu, const int* live,
                              const LiveCounts* cnt, float* x_out, int* cu_out,
                              int* live_out, int d, int rows_ub, int nlive_ub,
                              hipStream_t s);

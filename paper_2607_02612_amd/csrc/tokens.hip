@@ -5,7 +5,8 @@
 
 namespace fusion {
 
-__global__ void init_kernel(float* __restrict__ x, float* __restrict__ size,
+__global__ void init_kernel(float* __restrict__ x, int* __restrict__ rmap,
+                            float* __restrict__ size,
                             int* __restrict__ origin, int* __restrict__ cu,
                             int* __restrict__ live, LiveCounts* cnt,
                             int* __restrict__ token_counts,
@@ -22,6 +23,7 @@ __global__ void init_kernel(float* __restrict__ x, float* __restrict__ size,
     if (t < rows) {
       size[t] = 1.0f;
       origin[t] = (int)(t % T0);
+      rmap[t] = (int)t;
     }
     if (t < (long)B * L) token_counts[t] = 0;
     if (t < cls_elems) {
@@ -37,7 +39,7 @@ __global__ void init_kernel(float* __restrict__ x, float* __restrict__ size,
   }
 }
 
-hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
+hipError_t launch_init(float* x, int* rmap, float* size, int* origin, int* cu, int* live,
                        LiveCounts* cnt, int* token_counts, const float* cls,
                        const float* pos, int B, int n0, int d, int L,
                        hipStream_t s) {
@@ -46,7 +48,7 @@ hipError_t launch_init(float* x, float* size, int* origin, int* cu, int* live,
   if ((long)B * L > work) work = (long)B * L;
   int blocks = (int)((work + 255) / 256);
   if (blocks > 4096) blocks = 4096;
-  init_kernel<<<blocks, 256, 0, s>>>(x, size, origin, cu, live, cnt,
+  init_kernel<<<blocks, 256, 0, s>>>(x, rmap, size, origin, cu, live, cnt,
                                      token_counts, cls, pos, B, n0, d, L);
   return hipGetLastError();
 }
@@ -90,7 +92,7 @@ template hipError_t launch_patchify<bf16_t>(const float*, bf16_t*, int, int, int
 // vector stores; the row arithmetic is ln_row_half.
 template <typename T>
 __global__ __launch_bounds__(256) void layernorm_kernel(
-    const float* __restrict__ x, const float* __restrict__ g,
+    const float* __restrict__ x, const int* __restrict__ rmap, const float* __restrict__ g,
     const float* __restrict__ bb, T* __restrict__ out, int d,
     const LiveCounts* cnt, const int* __restrict__ cu,
     const int* __restrict__ live, int cls_only, int* exit_block, int L) {
@@ -98,13 +100,13 @@ __global__ __launch_bounds__(256) void layernorm_kernel(
   const int row = blockIdx.x * 8 + (threadIdx.x >> 5);
   const int nrows = cls_only ? cnt->nlive : cnt->M;
   if (row >= nrows) return;
-  const size_t src = cls_only ? (size_t)cu[row] : (size_t)row;
+  const size_t src = (size_t)rmap[cls_only ? cu[row] : row];
   ln_row_half<T>(x + src * d, d, lane & 31, g, bb, out + (size_t)row * d, nullptr);
   if (exit_block && (lane & 31) == 0) exit_block[live[row]] = L;
 }
 
 template <typename T>
-hipError_t launch_layernorm(const float* x, const float* g, const float* b,
+hipError_t launch_layernorm(const float* x, const int* rmap, const float* g, const float* b,
                             T* out, int d, const LiveCounts* cnt,
                             const int* cu, const int* live, int cls_only,
                             int rows_ub, int* exit_block, int L,
@@ -112,13 +114,15 @@ hipError_t launch_layernorm(const float* x, const float* g, const float* b,
   if (rows_ub <= 0) return hipSuccess;
   if (d > 4 * 32 * LN_MAXV || d % 4 != 0) return hipErrorInvalidValue;
   layernorm_kernel<T><<<(rows_ub + 7) / 8, 256, 0, s>>>(
-      x, g, b, out, d, cnt, cu, live, cls_only, exit_block, L);
+      x, rmap, g, b, out, d, cnt, cu, live, cls_only, exit_block, L);
   return hipGetLastError();
 }
-template hipError_t launch_layernorm<float>(const float*, const float*, const float*, float*, int,
+template hipError_t launch_layernorm<float>(const float*, const int*, const float*, const float*,
+                                            float*, int,
                                             const LiveCounts*, const int*, const int*, int, int,
                                             int*, int, hipStream_t);
-template hipError_t launch_layernorm<bf16_t>(const float*, const float*, const float*, bf16_t*,
+template hipError_t launch_layernorm<bf16_t>(const float*, const int*, const float*, const float*,
+                                             bf16_t*,
                                              int, const LiveCounts*, const int*, const int*, int,
                                              int, int*, int, hipStream_t);
 
@@ -134,7 +138,7 @@ template hipError_t launch_layernorm<bf16_t>(const float*, const float*, const f
 constexpr int POOL_MAXV = 3;  // 16-byte pieces per lane (d <= 768)
 template <typename T>
 __global__ __launch_bounds__(256) void pool_ln_kernel(
-    const float* __restrict__ x, const float* __restrict__ size,
+    const float* __restrict__ x, const int* __restrict__ rmap, const float* __restrict__ size,
     const int* __restrict__ cu, const LiveCounts* cnt,
     const float* __restrict__ g, const float* __restrict__ bb,
     T* __restrict__ out, int d) {
@@ -151,7 +155,7 @@ __global__ __launch_bounds__(256) void pool_ln_kernel(
   float den = 0.f;
   for (int t = 1 + wave; t < Tn; t += 4) {
     const float st = size[base + t];
-    const float4* xr = (const float4*)(x + (size_t)(base + t) * d);
+    const float4* xr = (const float4*)(x + (size_t)rmap[base + t] * d);
 #pragma unroll
     for (int k = 0; k < POOL_MAXV; k++) {
       const int q = lane + 64 * k;
@@ -182,22 +186,22 @@ __global__ __launch_bounds__(256) void pool_ln_kernel(
 }
 
 template <typename T>
-hipError_t launch_pool_ln(const float* x, const float* size, const int* cu,
+hipError_t launch_pool_ln(const float* x, const int* rmap, const float* size, const int* cu,
                           const LiveCounts* cnt, const float* g, const float* b,
                           T* out, int d, int nlive_ub, hipStream_t s) {
   if (nlive_ub <= 0) return hipSuccess;
   if (d % 4 != 0 || d > 4 * 64 * POOL_MAXV) return hipErrorInvalidValue;
-  pool_ln_kernel<T><<<nlive_ub, 256, 0, s>>>(x, size, cu, cnt, g, b, out, d);
+  pool_ln_kernel<T><<<nlive_ub, 256, 0, s>>>(x, rmap, size, cu, cnt, g, b, out, d);
   return hipGetLastError();
 }
-template hipError_t launch_pool_ln<float>(const float*, const float*, const int*,
+template hipError_t launch_pool_ln<float>(const float*, const int*, const float*, const int*,
                                           const LiveCounts*, const float*, const float*,
                                           float*, int, int, hipStream_t);
-template hipError_t launch_pool_ln<bf16_t>(const float*, const float*, const int*,
+template hipError_t launch_pool_ln<bf16_t>(const float*, const int*, const float*, const int*,
                                            const LiveCounts*, const float*, const float*,
                                            bf16_t*, int, int, hipStream_t);
 
-__global__ void copy_state_kernel(const float* __restrict__ x, const int* cu,
+__global__ void copy_state_kernel(const float* __restrict__ x, const int* rmap, const int* cu,
                                   const int* live, const LiveCounts* cnt,
                                   float* __restrict__ x_out, int* cu_out,
                                   int* live_out, int d) {
@@ -205,13 +209,13 @@ __global__ void copy_state_kernel(const float* __restrict__ x, const int* cu,
   const long n = (long)cnt->M * d;
   for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < n;
        t += (long)gridDim.x * blockDim.x)
-    x_out[t] = x[t];
+    x_out[t] = x[(size_t)rmap[t / d] * d + t % d];
   const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (t <= nl) cu_out[t] = cu[t];
   if (t < nl) live_out[t] = live[t];
 }
 
-hipError_t launch_copy_state(const float* x, const int* cu, const int* live,
+hipError_t launch_copy_state(const float* x, const int* rmap, const int* cu, const int* live,
                              const LiveCounts* cnt, float* x_out, int* cu_out,
                              int* live_out, int d, int rows_ub, int nlive_ub,
                              hipStream_t s) {
@@ -220,7 +224,7 @@ hipError_t launch_copy_state(const float* x, const int* cu, const int* live,
   const int need = (nlive_ub + 1 + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (blocks < need) blocks = need;
-  copy_state_kernel<<<blocks, 256, 0, s>>>(x, cu, live, cnt, x_out, cu_out,
+  copy_state_kernel<<<blocks, 256, 0, s>>>(x, rmap, cu, live, cnt, x_out, cu_out,
                                            live_out, d);
   return hipGetLastError();
 }
