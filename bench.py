@@ -101,10 +101,11 @@ def kernel_work(cfg, counts):
         # block and LN1 of block 1 (later LN1s are written by the compaction)
         "layernorm": {"flop": 0.0, "byte": float((M * d * (4 + 2)).sum() + M[0] * d * (4 + 2))},
         # adapt: read the sample's fp32 rows and sizes, write the merged rows
-        # back; compaction after block b: read and write the rows kept for
-        # block b + 1 (x, size, origin) and write their LN1 (bf16)
+        # back; compaction after block b: read the rows kept for block b + 1
+        # (fp32 row, row id, size, origin), write their LN1 (bf16) and their
+        # row id, size and origin (the fp32 rows themselves stay in place)
         "adapt": {"flop": 0.0, "byte": float((M * (d * 4 + 8) * 2).sum())},
-        "compact": {"flop": 0.0, "byte": float((M[1:] * ((d * 4 + 8) * 2 + d * 2)).sum())},
+        "compact": {"flop": 0.0, "byte": float((M[1:] * ((d * 4 + 12) + (d * 2 + 12))).sum())},
     }
     return w
 
