@@ -176,3 +176,17 @@ def test_capacity_and_argument_errors(torch_cuda):
     assert ei.value.code == -1
     with pytest.raises(FusionError):
         m.set_router_strength(-1.0)
+
+
+def test_residual_stream_capacity_limit(torch_cuda):
+    """create refuses a max_batch whose fp32 residual stream (max_batch x
+    (N0 + 1) x d elements, addressed with 32-bit offsets) would exceed 2^31
+    elements, with FUSION_E_CAPACITY (before the workspace is allocated)."""
+    from paper_2607_02612_amd import FusionError
+    cfg, W, _ = pu.make("deit_s_384", batch=1)
+    n0 = (cfg["img"] // cfg["patch"]) ** 2
+    limit = (2**31 - 1) // ((n0 + 1) * cfg["d"])
+    print(f"[capacity] deit_s_384: N0 + 1 = {n0 + 1}, d = {cfg['d']}, limit {limit}", flush=True)
+    with pytest.raises(FusionError) as ei:
+        pu.gpu_model(cfg, W, limit + 1)
+    assert ei.value.code == -3
