@@ -102,19 +102,19 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // waves, 2x2; 64: 2 waves side by side), each wave a 64x64 sub-tile of 2x2
 // v_mfma_f32_32x32x16_bf16 blocks.
 //
-// K is consumed in steps of KSV = 32 (three LDS stages) or 64 (two stages,
-// for long K).  A and W tiles reach LDS through the gfx950 asynchronous
+// K is consumed in steps of KSV = 32 through a ring of three LDS stages
+// (64-wide steps with two stages measured slower on every shape, long K
+// included).  A and W tiles reach LDS through the gfx950 asynchronous
 // global->LDS path (global_load_lds_dwordx4): each wave-wide instruction
-// writes 64 lanes x 16 bytes contiguously, i.e. 16 rows of 64 bytes or 8
-// rows of 128 bytes, without passing through VGPRs, so later K steps are in
+// writes 64 lanes x 16 bytes contiguously, i.e. 16 rows of 64 bytes,
+// without passing through VGPRs, so later K steps are in
 // flight while the matrix cores work on the current one (two or three
 // workgroups share a CU and cover each other's load latency).  The loads
 // are issued from inline assembly and their completion is awaited with
 // explicit vmcnt counts (a compiler-visible LDS DMA would make every LDS
 // read wait for all outstanding loads).  The 16-byte chunks of a staged row
-// are XOR-permuted (by (row / 4) % 4 for 64-byte rows, (row / 2) % 8 for
-// 128-byte rows), which makes the per-lane 16-byte operand reads of 16
-// consecutive rows hit 16 disjoint bank groups.  Rows past M or N are
+// are XOR-permuted by (row / 4) % 4, which makes the per-lane 16-byte
+// operand reads of 16 consecutive rows hit 16 disjoint bank groups.  Rows past M or N are
 // clamped to the last valid row for the loads (every address stays in
 // bounds) and masked in the epilogue.
 //
@@ -135,14 +135,8 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 constexpr int NB = 128;
 constexpr int NXCD = 8;
 
-#ifndef GEMM_BIG_TILES
-#define GEMM_BIG_TILES 1
-#endif
-
-template <int KSV>
-__device__ __forceinline__ int kslot(int r, int c) {
-  return KSV == 32 ? (c ^ ((r >> 2) & 3)) : (c ^ ((r >> 1) & 7));
-}
+// 16-byte chunk c of staged row r (64-byte rows: four chunks)
+__device__ __forceinline__ int kslot(int r, int c) { return c ^ ((r >> 2) & 3); }
 
 __device__ __forceinline__ void dma16(const void* gptr, unsigned lds_byte_addr) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
@@ -154,12 +148,13 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // MB = 256 (8 waves, 4x2), 128 (4 waves, 2x2) or 64 (2 waves, 1x2) rows per
-// tile.  KSV = K step.
+// tile.  KSV = K step (32).
 template <int EPI, int MB, int KSV>
-__global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) void gemm_mfma_bf16(
+__global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
     int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
-  constexpr int KS = KSV, NSTG = KSV == 64 ? 2 : 3;
+  static_assert(KSV == 32, "K step of 32");
+  constexpr int KS = KSV, NSTG = 3;
   constexpr int ROWB = KS * 2;                        // bytes per staged row
   constexpr int CPR = KS / 8;                         // 16-byte chunks per staged row
   constexpr int RPI = 64 / CPR;                       // rows per DMA instruction
@@ -197,7 +192,7 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
     const int q = wave * DMA_PER_WAVE + u;
     const bool isA = q < MB / RPI;
     const int r = (isA ? q : q - MB / RPI) * RPI + lane / CPR;
-    const int chunk = kslot<KSV>(r, lane % CPR);
+    const int chunk = kslot(r, lane % CPR);
     if (isA) {
       const int gr = min(m0 + r, M - 1);
       src[u] = A + (size_t)gr * lda + chunk * 8;
@@ -239,12 +234,12 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
 #pragma unroll
       for (int i = 0; i < 2; i++) {
         const int r = wm * 64 + i * 32 + (lane & 31);
-        a[i] = *(const bf16x8_t*)(Ab + r * ROWB + (kslot<KSV>(r, c) << 4));
+        a[i] = *(const bf16x8_t*)(Ab + r * ROWB + (kslot(r, c) << 4));
       }
 #pragma unroll
       for (int j = 0; j < 2; j++) {
         const int r = wn * 64 + j * 32 + (lane & 31);
-        b[j] = *(const bf16x8_t*)(Bb + r * ROWB + (kslot<KSV>(r, c) << 4));
+        b[j] = *(const bf16x8_t*)(Bb + r * ROWB + (kslot(r, c) << 4));
       }
       // transposed product: acc[i][j] holds C^T, so lane l owns output row
       // m = .. + (l % 32) and columns n = .. + 8 (q / 4) + 4 (l / 32) + q % 4
@@ -304,8 +299,8 @@ __global__ __launch_bounds__(MB / 64 * 128, (MB == 128 && KSV == 32) ? 3 : 1) vo
     // (512-byte rows, 16-byte chunk c of row r at c ^ (r % 32)), then the
     // workgroup adds them to x with whole-row accesses (32 lanes per
     // 512-byte row segment) instead of 16-byte pieces of 32 rows per
-    // instruction.  RR rows per round: all 128 when the drained ring holds
-    // 64 KB (K step 64), else two rounds of 64.
+    // instruction.  RR rows per round: the whole tile when the drained ring
+    // holds it (64-row tiles), else rounds of 64 rows.
     constexpr int RR = NSTG * STGB >= MB * NB * 4 ? MB : 64;
     float* x = (float*)e.out;
 #pragma unroll
@@ -455,7 +450,7 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   // half the barriers) measured slower on every shape here, long K included
   // (not for the GELU epilogue, whose vector work overlaps better with
   // three 4-wave workgroups per CU than with two 8-wave ones)
-  const bool big = GEMM_BIG_TILES && e.mode != EPI_GELU &&
+  const bool big = e.mode != EPI_GELU &&
                    (long)((M_ub + 255) / 256) * n_nt >= 1024;
   const int mb = small ? 64 : big ? 256 : 128;
   const int n_mt = (M_ub + mb - 1) / mb;
