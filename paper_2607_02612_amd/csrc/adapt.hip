@@ -113,18 +113,14 @@ __device__ __forceinline__ int rank_lanes(int n) {
   return P;
 }
 
-// Split a float into bf16 hi + lo with hi + lo = v to about 2^-17 relative.
-__device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
-  hi = f32_to_bf16(v);
-  lo = f32_to_bf16(v - bf16_to_f32(hi));
-}
-
 // Cosine similarities of the A tokens (even patch slots) with the B tokens
 // (odd slots) of one sample, and the best B for every A.
 //
 // One pass over the features in chunks of SKC, double-buffered in LDS.
-// Every thread owns a fixed set of (row, 4-feature) slots: the A rows of the
-// pass first, then the B rows (addresses clamped to the last real row, so
+// The token rows are read from x through prow (the sample's physical row of
+// each token slot).  Every thread owns a fixed set of (row, 4-feature)
+// slots: the A rows of the pass first, then the B rows (clamped to the last
+// real row, so
 // the loads need no branch; padding rows only feed outputs that are never
 // read).  The loads run two chunks ahead in two register sets.  A chunk's
 // values are split into bf16 hi + lo (hi = RNE(v), lo = RNE(v - hi)), with

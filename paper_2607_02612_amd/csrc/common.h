@@ -80,23 +80,7 @@ __device__ __forceinline__ int wave_sum_i(int v) {
   return v;
 }
 
-// Block-wide sum for blockDim.x == 256 (4 waves); `red` holds >= 4 floats.
-__device__ __forceinline__ float block_sum256(float v, float* red) {
-  v = wave_sum(v);
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  __syncthreads();
-  if (l == 0) red[w] = v;
-  __syncthreads();
-  return red[0] + red[1] + red[2] + red[3];
-}
-__device__ __forceinline__ float block_max256(float v, float* red) {
-  v = wave_max(v);
-  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  __syncthreads();
-  if (l == 0) red[w] = v;
-  __syncthreads();
-  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-}
+// Block-wide integer sum for blockDim.x == 256 (4 waves); `red` holds >= 4 ints.
 __device__ __forceinline__ int block_sum256_i(int v, int* red) {
   v = wave_sum_i(v);
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
