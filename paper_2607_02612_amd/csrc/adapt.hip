@@ -19,20 +19,23 @@ constexpr int AD_TMAX = 640;  // tokens per sample (CLS included), largest size 
 constexpr int AD_NT = 512;    // threads per workgroup (8 waves)
 
 // Size classes of the per-sample kernel: TMAX tokens (CLS included), so
-// |A| = ceil(N/2) and |B| = floor(N/2) are at most TMAX/2.
+// |A| = ceil(N/2) and |B| = floor(N/2) are at most TMAX/2.  The smallest
+// class (T <= 128, picked from the host's token bound of the block) stages
+// 64 features per chunk: its chunk loop is latency-bound, and half the
+// chunks halve the barriers.
 template <int TMAX_> struct AdSize {
   static constexpr int TMAX = TMAX_;
   static constexpr int AMAX = TMAX_ / 2;
   static constexpr int BMAX = TMAX_ / 2;
-  static constexpr int SKC = 32;               // features per chunk (one MFMA K step)
+  static constexpr int SKC = TMAX_ <= 128 ? 64 : 32;  // features per chunk (MFMA K steps of 32)
   static constexpr int SKP = SKC + 8;          // padded LDS row (bf16)
   // similarity wave layout: WC column groups of B tiles, AD_NT / 64 / WC
   // groups of 32 A rows; SAG A rows per pass
-  static constexpr int WC = TMAX_ <= 256 ? 2 : 4;
+  static constexpr int WC = TMAX_ <= 128 ? 4 : TMAX_ <= 256 ? 2 : 4;
   static constexpr int SAG = 32 * (AD_NT / 64 / WC);
   static constexpr int NBT = BMAX / 16;        // B tiles of 16 rows
   static constexpr int NBW = NBT / WC;         // B tiles per wave
-  static constexpr int BG = TMAX_ <= 256 ? 4 : 5;  // B tiles per group of the MFMA loop
+  static constexpr int BG = TMAX_ <= 128 ? 1 : TMAX_ <= 256 ? 4 : 5;  // B tiles per MFMA group
   static constexpr int SPT = ((SAG + BMAX) * (SKC / 4) + AD_NT - 1) / AD_NT;  // slots / thread
 };
 
@@ -148,7 +151,7 @@ __device__ void similarity_argmax(const float* __restrict__ x, const int* prow, 
   constexpr int SKC = Z::SKC, SKP = Z::SKP, SPT = Z::SPT, NBW = Z::NBW, BG = Z::BG;
   constexpr int SAG = Z::SAG, WC = Z::WC, BMAX = Z::BMAX;
   constexpr int Q = SKC / 4;  // 16-byte slots per row and chunk
-  static_assert(SKC == 32, "one MFMA K step per chunk");
+  static_assert(SKC % 32 == 0, "whole MFMA K steps per chunk");
   static_assert(SPT * AD_NT == (SAG + BMAX) * Q, "slots must tile the staged rows exactly");
   static_assert(NBW % BG == 0 && NBW * WC == Z::NBT, "wave layout: B tiles split evenly");
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -209,37 +212,40 @@ __device__ void similarity_argmax(const float* __restrict__ x, const int* prow, 
     const bool act = ag + 32 * wr < nA && wc * NBW < nbt;
     auto mfma = [&](int buf) {
       if (!act) return;
-      bf16x8_t ah[2], al[2];
 #pragma unroll
-      for (int i = 0; i < 2; i++) {
-        const int row = buf * SAG + 32 * wr + 16 * i + c;
-        ah[i] = *(const bf16x8_t*)(Ahi + row * SKP + 8 * g);
-        al[i] = *(const bf16x8_t*)(Alo + row * SKP + 8 * g);
-      }
+      for (int kk = 0; kk < SKC / 32; kk++) {
+        bf16x8_t ah[2], al[2];
 #pragma unroll
-      for (int t0 = 0; t0 < NBW; t0 += BG) {
-        bf16x8_t bh[BG], bl[BG];
-#pragma unroll
-        for (int j = 0; j < BG; j++) {
-          const int row = buf * BMAX + (wc * NBW + t0 + j) * 16 + c;
-          bh[j] = *(const bf16x8_t*)(Bhi + row * SKP + 8 * g);
-          bl[j] = *(const bf16x8_t*)(Blo + row * SKP + 8 * g);
+        for (int i = 0; i < 2; i++) {
+          const int row = buf * SAG + 32 * wr + 16 * i + c;
+          ah[i] = *(const bf16x8_t*)(Ahi + row * SKP + 32 * kk + 8 * g);
+          al[i] = *(const bf16x8_t*)(Alo + row * SKP + 32 * kk + 8 * g);
         }
 #pragma unroll
-        for (int j = 0; j < BG; j++)
+        for (int t0 = 0; t0 < NBW; t0 += BG) {
+          bf16x8_t bh[BG], bl[BG];
 #pragma unroll
-          for (int i = 0; i < 2; i++)
-            acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[j], ah[i], acc[i][t0 + j], 0, 0, 0);
+          for (int j = 0; j < BG; j++) {
+            const int row = buf * BMAX + (wc * NBW + t0 + j) * 16 + c;
+            bh[j] = *(const bf16x8_t*)(Bhi + row * SKP + 32 * kk + 8 * g);
+            bl[j] = *(const bf16x8_t*)(Blo + row * SKP + 32 * kk + 8 * g);
+          }
 #pragma unroll
-        for (int j = 0; j < BG; j++)
+          for (int j = 0; j < BG; j++)
 #pragma unroll
-          for (int i = 0; i < 2; i++)
-            acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl[j], ah[i], acc[i][t0 + j], 0, 0, 0);
+            for (int i = 0; i < 2; i++)
+              acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[j], ah[i], acc[i][t0 + j], 0, 0, 0);
 #pragma unroll
-        for (int j = 0; j < BG; j++)
+          for (int j = 0; j < BG; j++)
 #pragma unroll
-          for (int i = 0; i < 2; i++)
-            acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[j], al[i], acc[i][t0 + j], 0, 0, 0);
+            for (int i = 0; i < 2; i++)
+              acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl[j], ah[i], acc[i][t0 + j], 0, 0, 0);
+#pragma unroll
+          for (int j = 0; j < BG; j++)
+#pragma unroll
+            for (int i = 0; i < 2; i++)
+              acc[i][t0 + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[j], al[i], acc[i][t0 + j], 0, 0, 0);
+        }
       }
     };
     // chunk kc: MFMAs on buffer kc & 1; chunk kc + 1 (in registers `nx`)
@@ -597,7 +603,9 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
 
 hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
-  if (a.n0 + 1 <= 256) {
+  if (a.T_ub <= 128 && a.d % AdSize<128>::SKC == 0) {
+    adapt_kernel<AdSize<128>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
+  } else if (a.n0 + 1 <= 256) {
     if (a.d % AdSize<256>::SKC != 0) return hipErrorInvalidValue;
     adapt_kernel<AdSize<256>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
   } else {

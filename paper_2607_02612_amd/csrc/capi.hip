@@ -495,7 +495,7 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
         a.keep = m->keep; a.newlen = m->newlen;
         a.tr_r = tr ? tr->r : nullptr; a.tr_m = tr ? tr->m : nullptr;
         a.tr_c = tr ? tr->c : nullptr; a.tr_merge = tr ? tr->merge_dst : nullptr;
-        a.nlive_ub = B;
+        a.nlive_ub = B; a.T_ub = T_ub;
         HIP_OR_FAIL(launch_adapt(a, s));
       }
       {

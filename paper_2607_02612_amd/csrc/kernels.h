@@ -118,6 +118,7 @@ struct AdaptArgs {
   float* tr_c;
   int* tr_merge;
   int nlive_ub;
+  int T_ub;  // host bound on the tokens of every live sample (CLS included)
 };
 hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s);
 
