@@ -211,6 +211,39 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
       for (int u = 0; u < DMA_PER_WAVE; u++)
         dma16(src[u] + st * KS, __builtin_amdgcn_readfirstlane(lds0 + st * STGB + dst[u]));
     }
+  // staged residual / patch epilogue: the first round's row-map entries and
+  // addend rows are fetched during the last two K steps, so that their
+  // latency overlaps the final MFMAs
+  constexpr bool STAGED = (EPI == EPI_RESID || EPI == EPI_PATCH) && MB <= 128;
+  constexpr int RR = NSTG * STGB >= MB * NB * 4 ? MB : 64;  // rows per epilogue round
+  constexpr int PER = RR * (NB / 4) / NT;                   // 16-byte pieces per thread
+  float4 xpre[STAGED ? PER : 1];
+  int ppre[STAGED ? PER : 1];
+  auto row_map = [&](int rb, int* prow) {
+#pragma unroll
+    for (int k = 0; k < PER; k++) {
+      const int idx = tid + k * NT;
+      const int m = min(m0 + rb + idx / (NB / 4), M - 1);
+      prow[k] = (EPI == EPI_RESID && e.rows) ? e.rows[m] : m;
+    }
+  };
+  auto addend = [&](int rb, const int* prow, float4* xv) {
+    // the residual row (x += ...) or, for the patch embedding, the position
+    // embedding of patch token 1 + j, whose output row is s (n0 + 1) + 1 + j
+    // for packed row r = s n0 + j
+#pragma unroll
+    for (int k = 0; k < PER; k++) {
+      const int idx = tid + k * NT;
+      const int r = idx / (NB / 4), ch = idx % (NB / 4);
+      const int m = min(m0 + rb + r, M - 1), n = min(n0 + ch * 4, N - 4);
+      if (EPI == EPI_RESID) {
+        xv[k] = *(const float4*)((const float*)e.out + (size_t)prow[k] * e.ldo + n);
+      } else {
+        const int pj = m - (m / e.n0) * e.n0;
+        xv[k] = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + n);
+      }
+    }
+  };
   for (int kt = 0; kt < nk; kt++) {
     // stage kt has landed once at most the later stages are outstanding
     if (NSTG > 2 && kt + NSTG - 2 < nk)
@@ -224,6 +257,10 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
 #pragma unroll
       for (int u = 0; u < DMA_PER_WAVE; u++)
         dma16(src[u] + kn * KS, __builtin_amdgcn_readfirstlane(sb + dst[u]));
+    }
+    if constexpr (STAGED) {
+      if (kt == max(nk - 2, 0)) row_map(0, ppre);
+      if (kt == nk - 1) addend(0, ppre, xpre);
     }
     const char* Ab = smem + (kt % NSTG) * STGB;
     const char* Bb = Ab + MB * ROWB;
@@ -301,7 +338,6 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
     // 512-byte row segment) instead of 16-byte pieces of 32 rows per
     // instruction.  RR rows per round: the whole tile when the drained ring
     // holds it (64-row tiles), else rounds of 64 rows.
-    constexpr int RR = NSTG * STGB >= MB * NB * 4 ? MB : 64;
     float* x = (float*)e.out;
 #pragma unroll
     for (int rb = 0; rb < MB; rb += RR) {
@@ -329,30 +365,17 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
         }
       }
       __syncthreads();
-      constexpr int PER = RR * (NB / 4) / NT;          // 16-byte pieces per thread
-      // the addend: the residual row (x += ...) or, for the patch
-      // embedding, the position embedding of patch token 1 + j, whose
-      // output row is s (n0 + 1) + 1 + j for packed row r = s n0 + j
-      // (residual rows through the row map, whose entries are fetched first)
       float4 xv[PER];
       int prow[PER];
+      if (rb == 0) {
 #pragma unroll
-      for (int k = 0; k < PER; k++) {
-        const int idx = tid + k * NT;
-        const int m = min(m0 + rb + idx / (NB / 4), M - 1);
-        prow[k] = (EPI == EPI_RESID && e.rows) ? e.rows[m] : m;
-      }
-#pragma unroll
-      for (int k = 0; k < PER; k++) {
-        const int idx = tid + k * NT;
-        const int r = idx / (NB / 4), ch = idx % (NB / 4);
-        const int m = min(m0 + rb + r, M - 1), n = min(n0 + ch * 4, N - 4);
-        if (EPI == EPI_RESID) {
-          xv[k] = *(const float4*)(x + (size_t)prow[k] * e.ldo + n);
-        } else {
-          const int pj = m - (m / e.n0) * e.n0;
-          xv[k] = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + n);
+        for (int k = 0; k < PER; k++) {
+          xv[k] = xpre[k];
+          prow[k] = ppre[k];
         }
+      } else {
+        row_map(rb, prow);
+        addend(rb, prow, xv);
       }
 #pragma unroll
       for (int k = 0; k < PER; k++) {
