@@ -118,8 +118,8 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // clamped to the last valid row for the loads (every address stays in
 // bounds) and masked in the epilogue.
 //
-// Epilogue: every load it needs (bias, residual or position rows) is issued
-// as one batch.  bf16 outputs are staged through LDS (the drained K ring) so
+// Epilogue: the accumulators start at the bias, and every load the epilogue
+// needs (residual or position rows) is issued as one batch.  bf16 outputs are staged through LDS (the drained K ring) so
 // that global stores are whole 256-byte row segments instead of 16-byte
 // pieces of 32 different rows; the fp32 residual update and the patch
 // embedding are staged the same way as fp32 rows (512-byte segments), on
@@ -175,13 +175,24 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) void*)smem;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
+  // the accumulators start at the bias of their columns (lane l owns columns
+  // n0 + wn 64 + 32 j + 8 (q / 4) + 4 (l / 32) + q % 4; columns past N, never
+  // stored, take a clamped bias), so no epilogue adds it
   f32x16_t acc[2][2];
 #pragma unroll
-  for (int i = 0; i < 2; i++)
+  for (int j = 0; j < 2; j++)
 #pragma unroll
-    for (int j = 0; j < 2; j++)
+    for (int q4 = 0; q4 < 4; q4++) {
+      const float4 bv =
+          *(const float4*)(e.bias + min(n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5), N - 4));
 #pragma unroll
-      for (int q = 0; q < 16; q++) acc[i][j][q] = 0.f;
+      for (int i = 0; i < 2; i++) {
+        acc[i][j][4 * q4 + 0] = bv.x;
+        acc[i][j][4 * q4 + 1] = bv.y;
+        acc[i][j][4 * q4 + 2] = bv.z;
+        acc[i][j][4 * q4 + 3] = bv.w;
+      }
+    }
 
   // this lane's source row and LDS slot for each of the wave's DMA
   // instructions (8-row blocks: A rows first, then W rows)
@@ -220,11 +231,15 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   float4 xpre[STAGED ? PER : 1];
   int ppre[STAGED ? PER : 1];
   auto row_map = [&](int rb, int* prow) {
+    // one uniform branch for the whole batch: a select per entry would make
+    // each load wait for every earlier memory access of the wave
+    if (EPI == EPI_RESID && e.rows) {
 #pragma unroll
-    for (int k = 0; k < PER; k++) {
-      const int idx = tid + k * NT;
-      const int m = min(m0 + rb + idx / (NB / 4), M - 1);
-      prow[k] = (EPI == EPI_RESID && e.rows) ? e.rows[m] : m;
+      for (int k = 0; k < PER; k++)
+        prow[k] = e.rows[min(m0 + rb + (tid + k * NT) / (NB / 4), M - 1)];
+    } else {
+#pragma unroll
+      for (int k = 0; k < PER; k++) prow[k] = min(m0 + rb + (tid + k * NT) / (NB / 4), M - 1);
     }
   };
   auto addend = [&](int rb, const int* prow, float4* xv) {
@@ -292,24 +307,16 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
     // bf16 tile -> LDS (256-byte rows, 16-byte chunk c stored at c ^ (row % 16))
     // -> global, 16 lanes per 256-byte row segment
     __syncthreads();
-    // the four bias vectors of a column block are loaded together (columns
-    // clamped into range, so no branch separates the loads from each other)
 #pragma unroll
     for (int j = 0; j < 2; j++) {
-      float4 bv[4];
-#pragma unroll
-      for (int q4 = 0; q4 < 4; q4++) {
-        const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
-        bv[q4] = *(const float4*)(e.bias + min(n0 + c, N - 4));
-      }
 #pragma unroll
       for (int i = 0; i < 2; i++) {
         const int r = wm * 64 + i * 32 + (lane & 31);
 #pragma unroll
         for (int q4 = 0; q4 < 4; q4++) {
           const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
-          float v0 = acc[i][j][4 * q4 + 0] + bv[q4].x, v1 = acc[i][j][4 * q4 + 1] + bv[q4].y;
-          float v2 = acc[i][j][4 * q4 + 2] + bv[q4].z, v3 = acc[i][j][4 * q4 + 3] + bv[q4].w;
+          float v0 = acc[i][j][4 * q4 + 0], v1 = acc[i][j][4 * q4 + 1];
+          float v2 = acc[i][j][4 * q4 + 2], v3 = acc[i][j][4 * q4 + 3];
           if (EPI == EPI_GELU) {
             v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
           }
@@ -331,8 +338,8 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
     return;
   }
   if ((EPI == EPI_RESID || EPI == EPI_PATCH) && MB <= 128) {
-    // residual update (and patch embedding) through LDS: (acc + bias) rows
-    // are staged in fp32
+    // residual update (and patch embedding) through LDS: the accumulator
+    // rows (bias included) are staged in fp32
     // (512-byte rows, 16-byte chunk c of row r at c ^ (r % 32)), then the
     // workgroup adds them to x with whole-row accesses (32 lanes per
     // 512-byte row segment) instead of 16-byte pieces of 32 rows per
@@ -345,12 +352,6 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
       if (wm * 64 >= rb && wm * 64 < rb + RR) {
 #pragma unroll
         for (int j = 0; j < 2; j++) {
-          float4 bv[4];
-#pragma unroll
-          for (int q4 = 0; q4 < 4; q4++) {
-            const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
-            bv[q4] = *(const float4*)(e.bias + min(n0 + c, N - 4));
-          }
 #pragma unroll
           for (int i = 0; i < 2; i++) {
             const int r = wm * 64 + i * 32 + (lane & 31) - rb;
@@ -358,8 +359,8 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
             for (int q4 = 0; q4 < 4; q4++) {
               const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
               *(float4*)(smem + r * (NB * 4) + (((c >> 2) ^ (r & 31)) << 4)) =
-                  make_float4(acc[i][j][4 * q4 + 0] + bv[q4].x, acc[i][j][4 * q4 + 1] + bv[q4].y,
-                              acc[i][j][4 * q4 + 2] + bv[q4].z, acc[i][j][4 * q4 + 3] + bv[q4].w);
+                  make_float4(acc[i][j][4 * q4 + 0], acc[i][j][4 * q4 + 1],
+                              acc[i][j][4 * q4 + 2], acc[i][j][4 * q4 + 3]);
             }
           }
         }
@@ -412,13 +413,12 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
     }
 #pragma unroll
     for (int j = 0; j < 2; j++) {
-      // all loads of the column block first (bias, and the residual or
-      // position rows), then the arithmetic and the stores
-      float4 bv[4], xv[4];
+      // all loads of the column block first (the residual or position
+      // rows), then the arithmetic and the stores
+      float4 xv[4];
 #pragma unroll
       for (int q4 = 0; q4 < 4; q4++) {
         const int nb = min(n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5), N - 4);
-        bv[q4] = *(const float4*)(e.bias + nb);
         if (EPI == EPI_RESID) xv[q4] = *(const float4*)((const float*)e.out + orow * e.ldo + nb);
         if (EPI == EPI_PATCH) xv[q4] = *(const float4*)(e.pos + (size_t)(1 + pj) * e.ldo + nb);
       }
@@ -426,8 +426,8 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
       for (int q4 = 0; q4 < 4; q4++) {
         const int nb = n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
         if (nb >= N) continue;
-        const float v0 = acc[i][j][4 * q4 + 0] + bv[q4].x, v1 = acc[i][j][4 * q4 + 1] + bv[q4].y;
-        const float v2 = acc[i][j][4 * q4 + 2] + bv[q4].z, v3 = acc[i][j][4 * q4 + 3] + bv[q4].w;
+        const float v0 = acc[i][j][4 * q4 + 0], v1 = acc[i][j][4 * q4 + 1];
+        const float v2 = acc[i][j][4 * q4 + 2], v3 = acc[i][j][4 * q4 + 3];
         float4* po = (float4*)((float*)e.out + orow * e.ldo + nb);
         if (EPI == EPI_RESID) {
           *po = make_float4(xv[q4].x + v0, xv[q4].y + v1, xv[q4].z + v2, xv[q4].w + v3);
