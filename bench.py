@@ -6,7 +6,11 @@ already resident in HBM.  Default workload: DeiT-S shape, batch 256, bf16,
 224x224 images, router strength 1; the headline line is taken at the
 0 %-early-exit threshold, and the 50 % and 90 % settings (thresholds from
 the oracle calibration in tests/golden/exit_thresholds.json) are reported
-alongside.
+alongside.  The K timed steps are kernel-by-kernel launches on one stream
+(--graph: replays of the step captured as one HIP graph after the warm-up
+steps); the headline setting is also timed in the other launch mode and
+reported under "timing", with an event between consecutive steps for the
+median and 10th / 90th percentile step times.
 
 Also reported (same JSON line):
   paper     the Tab. I instantiation (DeiT-S, M = {3,5,7}, E = {8,10} with
@@ -21,7 +25,7 @@ Also reported (same JSON line):
 Prints one JSON line.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu]
-                       [--no-paper] [--headline-only]
+                       [--no-paper] [--headline-only] [--graph]
 """
 from __future__ import annotations
 
@@ -408,6 +412,10 @@ def main():
                     help="time only the 0 %% early-exit setting (for profiler runs)")
     ap.add_argument("--no-paper", action="store_true",
                     help="skip the Tab. I / Tab. VII / batch-sweep sections")
+    ap.add_argument("--graph", action="store_true",
+                    help="headline from replays of the step captured as one HIP "
+                         "graph (default: kernel-by-kernel launches; the other "
+                         "mode is timed too and reported under 'timing')")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 256 MiB device-to-device copy, whose HBM "
                          "counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -436,24 +444,40 @@ def main():
     x = torch.from_numpy(imgs).cuda()
     out = model.alloc_outputs(B)
 
-    def timed(delta):
+    def timed(delta, graph):
+        # the thresholds are kernel arguments: set them, then capture the step
         model.set_exit_thresholds([delta] * len(cfg["exits"]))
         for _ in range(args.warmup):
             model.run(x, out=out)
         torch.cuda.synchronize()
-        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        step = lambda: model.run(x, out=out)
+        if graph:
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                model.run(x, out=out)
+            step = graph.replay
+            step()
+            torch.cuda.synchronize()
+        # one event between consecutive steps: the mean over the K steps is
+        # the first-to-last interval / K, and the per-step intervals give the
+        # median and the 10th / 90th percentiles
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         t0 = time.perf_counter()
-        s.record()
-        for _ in range(args.steps):
-            model.run(x, out=out)
-        e.record()
+        ev[0].record()
+        for i in range(args.steps):
+            step()
+            ev[i + 1].record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        ms = s.elapsed_time(e) / args.steps
+        ms = ev[0].elapsed_time(ev[-1]) / args.steps
+        per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)])
         counts = out[2].cpu().numpy()
         eb = out[1].cpu().numpy()
         fl = executed_flops(cfg, counts, eb)
         return dict(ms=ms, wall_ms=1e3 * wall / args.steps, img_s=B / (ms / 1e3),
+                    step_ms={"median": float(np.median(per)),
+                             "p10": float(np.percentile(per, 10)),
+                             "p90": float(np.percentile(per, 90))},
                     flops=fl, pct_peak=100.0 * fl / (ms / 1e3) / BF16_PEAK,
                     early_exit=float((eb < cfg["L"]).mean()),
                     mean_tokens=float(counts[counts > 0].mean()), counts=counts)
@@ -470,8 +494,9 @@ def main():
     for e_rate in sorted(th):
         if args.headline_only and e_rate != 0.0:
             continue
-        sweep[e_rate] = timed(th[e_rate])
+        sweep[e_rate] = timed(th[e_rate], args.graph)
     head = sweep[0.0]
+    other = timed(th[0.0], not args.graph)
 
     # per-kernel timing (HIP events around each launch, separate pass)
     model.set_exit_thresholds([th[0.0]] * len(cfg["exits"]))
@@ -534,10 +559,16 @@ def main():
                                f"0% early exit",
                    "batch": B, "image": cfg["img"], "tokens": cfg["N0"] + 1,
                    "d": cfg["d"], "heads": cfg["H"], "layers": cfg["L"]},
+        "timing": {"launch": "hip_graph" if args.graph else "eager",
+                   "step_ms": head["step_ms"],
+                   ("eager" if args.graph else "hip_graph"):
+                       {"ms_per_step": other["ms"], "images_per_s": other["img_s"],
+                        "step_ms": other["step_ms"]}},
         "pct_bf16_peak_executed": head["pct_peak"],
         "executed_gflop_per_image": head["flops"] / B / 1e9,
         "exit_sweep": {f"{int(100 * e)}%": {"threshold": th[e], "images_per_s": r["img_s"],
                                              "ms_per_step": r["ms"],
+                                             "step_ms": r["step_ms"],
                                              "pct_bf16_peak_executed": r["pct_peak"],
                                              "measured_early_exit": r["early_exit"],
                                              "executed_gflop_per_image": r["flops"] / B / 1e9}
