@@ -141,6 +141,37 @@ def measured_traffic(kernel):
     return entry["bytes_per_launch"]
 
 
+def measured_peaks(torch):
+    """What the box itself reaches, beside the vendor peaks: HBM as a 1 GiB
+    device-to-device copy (bytes read + written over the copy time), MFMA as
+    a 8192^3 bf16 GEMM through torch (the vendor library), best of 20."""
+    src = torch.empty(256 << 20, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    b = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    c = torch.empty(8192, 8192, device="cuda", dtype=torch.bfloat16)
+
+    def best(fn, reps=20):
+        for _ in range(3):
+            fn()
+        t = []
+        for _ in range(reps):
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            fn()
+            e.record()
+            e.synchronize()
+            t.append(s.elapsed_time(e) / 1e3)
+        return min(t)
+
+    t_copy = best(lambda: dst.copy_(src))
+    t_mm = best(lambda: torch.matmul(a, b, out=c))
+    del src, dst, a, b, c
+    return {"hbm_copy_gbps": 2 * (1 << 30) / t_copy / 1e9,
+            "bf16_gemm_tflops": 2 * 8192 ** 3 / t_mm / 1e12,
+            "method": "1 GiB device copy; 8192^3 bf16 torch.matmul; best of 20"}
+
+
 def cpu_baseline(cfg, W, imgs, n):
     """The oracle on the first n images (bounded sample), images/s."""
     from oracle import fusion_oracle as fo
@@ -577,6 +608,19 @@ def main():
         "step_roofline": step_roof,
         "kernels": kernels,
     }
+    if not args.headline_only:
+        # (not in profiler runs: its copy would be taken for the counter
+        # calibration copy)
+        mp = measured_peaks(torch)
+        line["measured_peaks"] = mp
+        if roofline["unit"] == "GB/s":
+            roofline["frac_of_measured"] = roofline["achieved"] / mp["hbm_copy_gbps"]
+        else:
+            roofline["frac_of_measured"] = roofline["achieved"] / mp["bf16_gemm_tflops"]
+        if "mfma_tflops" in roofline:
+            roofline["frac_of_measured_gemm"] = roofline["mfma_tflops"] / mp["bf16_gemm_tflops"]
+        line["pct_measured_gemm_peak_executed"] = (
+            100.0 * head["flops"] / (head["ms"] / 1e3) / (mp["bf16_gemm_tflops"] * 1e12))
     if not (args.no_paper or args.headline_only):
         model.close()
         energy = EnergyMeter()
