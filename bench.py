@@ -180,17 +180,32 @@ def cpu_baseline(cfg, W, imgs, n):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count() or 1
-    Wp = fo.prepare_weights(W, "bf16emu")
-    fo.run_sample(imgs[0], Wp, cfg, "bf16emu")          # warm-up image
-    t0 = time.perf_counter()
-    for i in range(n):
-        fo.run_sample(imgs[i], Wp, cfg, "bf16emu")
-    dt = time.perf_counter() - t0
-    return {"value": n / dt, "unit": "images/s", "cores": int(cores),
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
+
+    def rate(mode, k):
+        Wp = fo.prepare_weights(W, mode)
+        fo.run_sample(imgs[0], Wp, cfg, mode)          # warm-up image
+        t0 = time.perf_counter()
+        for i in range(k):
+            fo.run_sample(imgs[i], Wp, cfg, mode)
+        return k / (time.perf_counter() - t0), time.perf_counter() - t0
+
+    v, dt = rate("bf16emu", n)
+    n32 = max(1, n // 4)
+    v32, dt32 = rate("fp32", n32)
+    return {"value": v, "unit": "images/s", "cores": int(cores),
             "kind": "oracle",
             "sample": f"first {n} of the {imgs.shape[0]} DeiT-S images, bf16emu "
                       f"mode, exits disabled, merge and prune at rho=1 "
-                      f"({dt:.1f} s wall)"}
+                      f"({dt:.1f} s wall)",
+            "fp32_mode": {"value": v32, "unit": "images/s",
+                          "sample": f"first {n32} images, fp32 mode ({dt32:.1f} s wall)"},
+            "host": {"cpu_model": model, "os_cpu_count": os.cpu_count()}}
 
 
 class EnergyMeter:
@@ -438,7 +453,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="deit_s")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-images", type=int, default=48)
+    ap.add_argument("--cpu-images", type=int, default=256)
     ap.add_argument("--headline-only", action="store_true",
                     help="time only the 0 %% early-exit setting (for profiler runs)")
     ap.add_argument("--no-paper", action="store_true",
