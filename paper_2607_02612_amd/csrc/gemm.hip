@@ -114,16 +114,19 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // explicit vmcnt counts (a compiler-visible LDS DMA would make every LDS
 // read wait for all outstanding loads).  The 16-byte chunks of a staged row
 // are XOR-permuted by (row / 4) % 4, which makes the per-lane 16-byte
-// operand reads of 16 consecutive rows hit 16 disjoint bank groups.  Rows past M or N are
-// clamped to the last valid row for the loads (every address stays in
-// bounds) and masked in the epilogue.
+// operand reads of 16 consecutive rows hit 16 disjoint bank groups.  Rows
+// past M or N are clamped to the last valid row for the loads (every
+// address stays in bounds) and masked in the epilogue.
 //
 // Epilogue: the accumulators start at the bias, and every load the epilogue
-// needs (residual or position rows) is issued as one batch.  bf16 outputs are staged through LDS (the drained K ring) so
-// that global stores are whole 256-byte row segments instead of 16-byte
-// pieces of 32 different rows; the fp32 residual update and the patch
-// embedding are staged the same way as fp32 rows (512-byte segments), on
-// tiles of up to 128 rows; fp32 logits and 256-row tiles write directly.
+// needs (residual or position rows) is issued as one batch; for the staged
+// fp32 epilogues the first round's row-map entries and addend rows are
+// fetched during the last two K steps.  bf16 outputs are staged through LDS
+// (the drained K ring) so that global stores are whole 256-byte row
+// segments instead of 16-byte pieces of 32 different rows; the fp32
+// residual update and the patch embedding are staged the same way as fp32
+// rows (512-byte segments), on tiles of up to 128 rows; fp32 logits and
+// 256-row tiles write directly.
 //
 // Tile order: blocks are dispatched round-robin over the 8 XCDs (block id %
 // 8); the linear id is remapped so that each XCD walks whole row panels (all
