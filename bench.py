@@ -486,6 +486,7 @@ def main():
     for wl in cal["workloads"]:
         if wl["workload"] == args.workload and wl["rho"] == 1.0:
             th = {float(k): v for k, v in wl["thresholds"].items()}
+    th.setdefault(0.0, 1.0)  # delta = 1: no exit (the 0 % setting where none is calibrated)
     model = FusionModel(blob.pack(cfg, W), B)
     x = torch.from_numpy(imgs).cuda()
     out = model.alloc_outputs(B)

@@ -3,7 +3,9 @@
 // per-head CLS attention row that scores tokens for pruning.
 //
 // Softmax uses the exact row maximum: the full score row of a query is held
-// (LDS or registers) before exponentiation.  E = exp(S - max), l = sum E in
+// (LDS or registers) before exponentiation, or, in the chunked MFMA kernel
+// for long samples, found by a first pass over the keys whose scores the
+// second pass recomputes bit for bit.  E = exp(S - max), l = sum E in
 // fp32, the stored probabilities E are rounded to the storage type before
 // they multiply V, and O = (round(E) V) / l.  The MFMA kernels evaluate the
 // exponent in base 2 with the hardware exp2: t = dot (scale log2 e) +
@@ -120,7 +122,8 @@ __global__ __launch_bounds__(256) void attention_valu(AttnArgs a) {
 // maximum and the row sum are reductions over the lane's registers plus two
 // xor-shuffles (lanes l, l^16, l^32, l^48 share a query).  Keys are streamed
 // through LDS in chunks of 64 (K row-major; V transposed to [dh][key]), so
-// any length up to 16 * MAXT keys fits.  For O = P V the lane's own
+// any length up to 16 * MAXT keys fits: one pass over the chunks for the
+// row maximum, a second for E, l and O.  For O = P V the lane's own
 // probabilities of key tiles 2p and 2p+1 form the MFMA A operand directly:
 // the 8 k-slots of lane l map to keys {32p + 4g + i, 32p + 16 + 4g + i}
 // (g = l/16, i < 4), and the V operand is read from the transposed chunk
@@ -132,7 +135,7 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int AKC = 64;            // keys per LDS chunk
 constexpr int AKS = 64 + 8;        // K chunk row stride (bf16), dh = 64
-constexpr int AVS = AKC + 8;       // V^T chunk row stride (bf16)
+constexpr int AVS = AKC + 4;       // V^T chunk row stride (bf16): an odd multiple of 8 bytes
 
 template <int MAXT>
 __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
@@ -171,121 +174,140 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
     }
   }
 
-  // ---- phase 1: S^T tiles for all keys
-  f32x4_t S[MAXT];
-#pragma unroll
-  for (int t = 0; t < MAXT; t++) S[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // Two passes over the key chunks, each holding one chunk's scores in
+  // registers (a whole score row would take 160 VGPRs at 640 keys and leave
+  // one wave per SIMD): the first finds the exact row maximum, the second
+  // recomputes the same scores (same MFMA operands and order, so the same
+  // bits), exponentiates them and accumulates l and round(E) V chunk by
+  // chunk in the key order of a single pass.
   const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
-  for (int ch = 0; ch < nch; ch++) {
-    __syncthreads();
-    // stage 64 keys x 64 dims (rows beyond T are zero)
-    for (int u = tid; u < AKC * 8; u += 256) {
-      const int r = u >> 3, cc = (u & 7) * 8;
-      const int key = ch * AKC + r;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (key < Tn) v = *(const uint4*)(kg + (size_t)key * ld + cc);
-      *(uint4*)(Ks + r * AKS + cc) = v;
-    }
-    __syncthreads();
+  const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
+  // stage 64 keys x 64 dims of K, and optionally V^T ([dim][key]); rows
+  // beyond T are zero
+  auto stage = [&](int ch, bool with_v) {
+    uint4 kv[AKC * 8 / 256], vv[AKC * 8 / 256];
 #pragma unroll
-    for (int t = 0; t < MAXT; t++) {
-      if ((t >> 2) == ch) {
-        const bf16_t* kr = Ks + ((t & 3) * 16 + c) * AKS + 8 * g;
-        const bf16x8_t k0 = *(const bf16x8_t*)kr;
-        const bf16x8_t k1 = *(const bf16x8_t*)(kr + 32);
-        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[0], S[t], 0, 0, 0);
-        S[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[1], S[t], 0, 0, 0);
+    for (int w = 0; w < AKC * 8 / 256; w++) {
+      const int u = tid + w * 256;
+      const int key = ch * AKC + (u >> 3), cc = (u & 7) * 8;
+      kv[w] = make_uint4(0, 0, 0, 0);
+      vv[w] = make_uint4(0, 0, 0, 0);
+      if (key < Tn) {
+        kv[w] = *(const uint4*)(kg + (size_t)key * ld + cc);
+        if (with_v) vv[w] = *(const uint4*)(vg + (size_t)key * ld + cc);
       }
     }
-  }
-
-  // ---- softmax with the exact row maximum (lane's query = q0 + c)
-  float mx = -INFINITY;
 #pragma unroll
-  for (int t = 0; t < MAXT; t++) {
+    for (int w = 0; w < AKC * 8 / 256; w++) {
+      const int u = tid + w * 256;
+      const int r = u >> 3, cc = (u & 7) * 8;
+      *(uint4*)(Ks + r * AKS + cc) = kv[w];
+      if (with_v) {
+        const bf16_t* e = (const bf16_t*)&vv[w];
 #pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const int key = t * 16 + 4 * g + j;
-      float v = -INFINITY;
-        if (t < nkt && key < Tn) v = fmaf(S[t][j], sc2, lnS[key]);
-      S[t][j] = v;
-      mx = fmaxf(mx, v);
+        for (int q = 0; q < 8; q++) Vt[(cc + q) * AVS + r] = e[q];
+      }
     }
-  }
-  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-  float ls = 0.f;
+  };
+  // base-2 scores of the chunk's four key tiles: lane (g, c) holds keys
+  // 16t + 4g + j of query q0 + c, with the key term; -inf past the keys
+  auto scores = [&](int ch, f32x4_t* s4) {
 #pragma unroll
-  for (int t = 0; t < MAXT; t++)
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const float e = (t < nkt) ? __builtin_amdgcn_exp2f(S[t][j] - mx) : 0.f;
-      S[t][j] = e;
-      ls += e;
-    }
-  ls += __shfl_xor(ls, 16, 64);
-  ls += __shfl_xor(ls, 32, 64);
-  const float rl = 1.0f / ls;
-
-  if (a.cls_scores && q0 == 0 && c == 0) {
-    float* cs = a.cls_scores + ((size_t)i * a.H + h) * a.tmax;
-#pragma unroll
-    for (int t = 0; t < MAXT; t++)
+    for (int tt = 0; tt < 4; tt++) {
+      const int t = 4 * ch + tt;
+      f32x4_t sv = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      if (t < MAXT) {
+        const bf16_t* kr = Ks + (tt * 16 + c) * AKS + 8 * g;
+        const bf16x8_t k0 = *(const bf16x8_t*)kr;
+        const bf16x8_t k1 = *(const bf16x8_t*)(kr + 32);
+        sv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[0], sv, 0, 0, 0);
+        sv = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[1], sv, 0, 0, 0);
+      }
 #pragma unroll
       for (int j = 0; j < 4; j++) {
         const int key = t * 16 + 4 * g + j;
-        if (t < nkt && key < Tn) cs[key] = S[t][j] * rl;
+        float v = -INFINITY;
+        if (t < nkt && key < Tn) v = fmaf(sv[j], sc2, lnS[key]);
+        s4[tt][j] = v;
       }
-  }
+    }
+  };
 
-  // ---- phase 2: O = round(E) V over key-tile pairs
+  // ---- pass 1: the exact row maximum
+  float mx = -INFINITY;
+  for (int ch = 0; ch < nch; ch++) {
+    __syncthreads();
+    stage(ch, false);
+    __syncthreads();
+    f32x4_t s4[4];
+    scores(ch, s4);
+#pragma unroll
+    for (int tt = 0; tt < 4; tt++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) mx = fmaxf(mx, s4[tt][j]);
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+
+  // ---- pass 2: E = exp2(s - max), l = sum E, O = round(E) V over key-tile
+  // pairs; the CLS query's E go out unnormalised and are scaled by 1 / l
+  // once l is known
+  const bool cls_lane = a.cls_scores && q0 == 0 && c == 0;
+  float* cs = a.cls_scores ? a.cls_scores + ((size_t)i * a.H + h) * a.tmax : nullptr;
+  float ls = 0.f;
   f32x4_t O[4];
 #pragma unroll
   for (int n = 0; n < 4; n++) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
   for (int ch = 0; ch < nch; ch++) {
     __syncthreads();
-    // stage V^T for 64 keys: Vt[dim][key]; keys beyond T are zero
-    for (int u = tid; u < AKC * 8; u += 256) {
-      const int r = u >> 3, cc = (u & 7) * 8;
-      const int key = ch * AKC + r;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (key < Tn) v = *(const uint4*)(vg + (size_t)key * ld + cc);
-      const bf16_t* e = (const bf16_t*)&v;
-#pragma unroll
-      for (int q = 0; q < 8; q++) Vt[(cc + q) * AVS + r] = e[q];
-    }
+    stage(ch, true);
     __syncthreads();
+    f32x4_t s4[4];
+    scores(ch, s4);
 #pragma unroll
-    for (int p = 0; p < (MAXT + 1) / 2; p++) {
-      if ((p >> 1) == ch) {
-        const int t0 = 2 * p, t1 = 2 * p + 1;
-        bf16x8_t pa;
+    for (int tt = 0; tt < 4; tt++) {
+      const int t = 4 * ch + tt;
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const float e = (t < nkt) ? __builtin_amdgcn_exp2f(s4[tt][j] - mx) : 0.f;
+        s4[tt][j] = e;
+        ls += e;
+        const int key = t * 16 + 4 * g + j;
+        if (cls_lane && t < nkt && key < Tn) cs[key] = e;
+      }
+    }
+#pragma unroll
+    for (int pp = 0; pp < 2; pp++) {
+      const int p = 2 * ch + pp, t1 = 2 * p + 1;
+      if (p < (MAXT + 1) / 2) {
+        union { bf16_t u[8]; bf16x8_t v; } cv;
 #pragma unroll
         for (int j = 0; j < 4; j++) {
-          pa[j] = (__bf16)0.f;
-          pa[4 + j] = (__bf16)0.f;
+          cv.u[j] = f32_to_bf16(s4[2 * pp][j]);
+          cv.u[4 + j] = f32_to_bf16(t1 < MAXT ? s4[2 * pp + 1][j] : 0.f);
         }
-        {
-          union { bf16_t u[8]; bf16x8_t v; } cv;
-#pragma unroll
-          for (int j = 0; j < 4; j++) {
-            cv.u[j] = f32_to_bf16(t0 < MAXT ? S[t0 < MAXT ? t0 : 0][j] : 0.f);
-            cv.u[4 + j] = f32_to_bf16(t1 < MAXT ? S[t1 < MAXT ? t1 : 0][j] : 0.f);
-          }
-          pa = cv.v;
-        }
-        const int kl = (p & 1) * 32 + 4 * g;  // key offset inside the chunk
+        const int kl = pp * 32 + 4 * g;  // key offset inside the chunk
 #pragma unroll
         for (int n = 0; n < 4; n++) {
           const bf16_t* vr = Vt + (n * 16 + c) * AVS + kl;
           union { uint2 u[2]; bf16x8_t v; } vb;
           vb.u[0] = *(const uint2*)vr;
           vb.u[1] = *(const uint2*)(vr + 16);
-          O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb.v, O[n], 0, 0, 0);
+          O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cv.v, vb.v, O[n], 0, 0, 0);
         }
       }
     }
+  }
+  ls += __shfl_xor(ls, 16, 64);
+  ls += __shfl_xor(ls, 32, 64);
+  const float rl = 1.0f / ls;
+  if (cls_lane) {
+    for (int t = 0; t < nkt; t++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int key = t * 16 + 4 * g + j;
+        if (key < Tn) cs[key] = cs[key] * rl;
+      }
   }
 
   // ---- normalise and store: lane holds O[q0 + 4g + j][16n + c]
@@ -327,7 +349,11 @@ __global__ __launch_bounds__(RES_NT, 4) void attention_mfma_res(AttnArgs a) {
   constexpr int TP = MAXT * 16;               // padded keys
   constexpr int NP = (MAXT + 1) / 2;          // key tile pairs
   constexpr int TPE = NP * 32;                // keys covered by tile pairs
-  constexpr int VTS = TPE + 8;                // V^T row stride (bf16)
+  // V^T row stride (bf16): TPE + 4 makes the byte stride an odd multiple of
+  // 8, which measured fastest for the 8-byte V^T reads and the transposing
+  // stores (attention 0.294 ms per step at DeiT-S batch 256, against 0.315
+  // for TPE + 8 or + 24, 0.377 for + 16 and 0.52 for TPE itself)
+  constexpr int VTS = TPE + 4;
   const int i = blockIdx.x, h = blockIdx.y;
   if (i >= a.cnt->nlive) return;
   const int base = a.cu[i], Tn = a.cu[i + 1] - base;
