@@ -183,11 +183,13 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
   const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
   const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
   // stage 64 keys x 64 dims of K, and optionally V^T ([dim][key]); rows
-  // beyond T are zero
-  auto stage = [&](int ch, bool with_v) {
-    uint4 kv[AKC * 8 / 256], vv[AKC * 8 / 256];
+  // beyond T are zero.  The global loads of a chunk (load) are issued one
+  // chunk ahead into registers and written to LDS (put) after the barrier
+  // that ends the previous chunk's reads.
+  constexpr int SW = AKC * 8 / 256;  // 16-byte pieces per thread and chunk
+  auto load = [&](int ch, bool with_v, uint4* kv, uint4* vv) {
 #pragma unroll
-    for (int w = 0; w < AKC * 8 / 256; w++) {
+    for (int w = 0; w < SW; w++) {
       const int u = tid + w * 256;
       const int key = ch * AKC + (u >> 3), cc = (u & 7) * 8;
       kv[w] = make_uint4(0, 0, 0, 0);
@@ -197,8 +199,10 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
         if (with_v) vv[w] = *(const uint4*)(vg + (size_t)key * ld + cc);
       }
     }
+  };
+  auto put = [&](bool with_v, const uint4* kv, const uint4* vv) {
 #pragma unroll
-    for (int w = 0; w < AKC * 8 / 256; w++) {
+    for (int w = 0; w < SW; w++) {
       const int u = tid + w * 256;
       const int r = u >> 3, cc = (u & 7) * 8;
       *(uint4*)(Ks + r * AKS + cc) = kv[w];
@@ -235,10 +239,13 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
 
   // ---- pass 1: the exact row maximum
   float mx = -INFINITY;
+  uint4 kv[SW], vv[SW];
+  load(0, false, kv, vv);
   for (int ch = 0; ch < nch; ch++) {
     __syncthreads();
-    stage(ch, false);
+    put(false, kv, vv);
     __syncthreads();
+    if (ch + 1 < nch) load(ch + 1, false, kv, vv);
     f32x4_t s4[4];
     scores(ch, s4);
 #pragma unroll
@@ -258,10 +265,12 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
   f32x4_t O[4];
 #pragma unroll
   for (int n = 0; n < 4; n++) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  load(0, true, kv, vv);
   for (int ch = 0; ch < nch; ch++) {
     __syncthreads();
-    stage(ch, true);
+    put(true, kv, vv);
     __syncthreads();
+    if (ch + 1 < nch) load(ch + 1, true, kv, vv);
     f32x4_t s4[4];
     scores(ch, s4);
 #pragma unroll
