@@ -44,7 +44,7 @@ Readings of the paper where it is silent (each also listed in the design doc):
       to C, on the CLS token; "pool_mlp" = the same MLP on the size-weighted
       mean of the patch tokens sum_t s_t z_t / sum_t s_t (CLS excluded; a
       sample without patch tokens pools to the zero vector), taken after the
-      block's merge (Sec. IV, exit-head description).
+      block's merge (Sec. IV-I, Parameter and Memory Overhead).
   exit: head_b as above, c = max softmax
       = 1 / sum_k exp(l_k - l_max); exit iff delta < 1 and c >= delta
       (Eq. 6-7).  Exited samples return head_b's logits.
@@ -179,17 +179,28 @@ def patch_embed(img, W, cfg, mode):
 def attention(x, s, Wb, cfg, mode, want_cls):
     """Multi-head self-attention on LN1(x); returns (O, cls_attn or None).
 
+    q|k|v = round(LN1(x) W_qkv^T + b_qkv), then ``attention_heads``.
+    """
+    h = _rnd(layer_norm(x, Wb["ln1_g"], Wb["ln1_b"]), mode)
+    qkv = _rnd(_mm(h, Wb["qkv_w"].T) + Wb["qkv_b"], mode)
+    return attention_heads(qkv, s, cfg["H"], cfg["prop_attn"], mode, want_cls)
+
+
+def attention_heads(qkv, s, H, prop_attn, mode, want_cls):
+    """Multi-head attention of one sample on its q|k|v rows [T, 3d]
+    (columns q | k | v, each head-major); returns (O rounded to the storage
+    type, cls_attn or None).
+
     S = (q k^T) * dh^-1/2 + ln(s_key) (proportional attention),
     E = exp(S - rowmax), l = rowsum(E), O = (round(E) V) / l.
     cls_attn[j] = mean over heads of E[0, j] / l[0] (float32, unrounded).
     """
-    d, H = cfg["d"], cfg["H"]
+    qkv = np.asarray(qkv, dtype=F32)
+    d = qkv.shape[1] // 3
     dh = d // H
-    h = _rnd(layer_norm(x, Wb["ln1_g"], Wb["ln1_b"]), mode)
-    qkv = _rnd(_mm(h, Wb["qkv_w"].T) + Wb["qkv_b"], mode)
     scale = F32(1.0 / math.sqrt(dh))
-    bias = np.log(s).astype(F32) if cfg["prop_attn"] else None
-    T = x.shape[0]
+    bias = np.log(s).astype(F32) if prop_attn else None
+    T = qkv.shape[0]
     O = np.empty((T, d), dtype=F32)
     cls_rows = []
     for hh in range(H):

@@ -89,7 +89,7 @@ CONFIGS = {
 }
 
 
-# Operating profiles of the paper workloads (Sec. IV, Profiles; Tab. I):
+# Operating profiles of the paper workloads (Sec. IV-A, Profiles; Tab. I):
 # per profile the exit thresholds delta_b and the target keep ratio tau_tgt;
 # the router strength is rho = (1 - tau_tgt) / (1 - tau_tgt(balanced)), the
 # rescaling of Eq. 5, which also scales the prune keep ratios.  balanced is
