@@ -25,9 +25,50 @@ def _stream_ptr(stream) -> int:
     return s.cuda_stream
 
 
-def _dev_f32(t: torch.Tensor, name: str):
-    if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous()):
-        raise ValueError(f"{name} must be a contiguous float32 GPU tensor")
+def _expect(t, name, shape, dtype, device):
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a tensor")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def check_run_args(info: dict, device: torch.device, images, out=None,
+                   trace=None) -> int:
+    """Host-side checks of fusion_run's buffers before any launch: a
+    wrong-resolution batch or an undersized output would make the kernels
+    read or write past the tensors.  Returns the batch size; raises
+    ValueError on any mismatch."""
+    if not isinstance(images, torch.Tensor) or images.dim() != 4:
+        raise ValueError("images must be a 4-d tensor [batch, channels, side, side]")
+    B = int(images.shape[0])
+    if B < 1:
+        raise ValueError("images holds no sample")
+    # (a batch above max_batch is the library's FUSION_E_CAPACITY)
+    S, C = info["img"], info["in_ch"]
+    _expect(images, "images", (B, C, S, S), torch.float32, device)
+    if out is not None:
+        if len(out) != 3:
+            raise ValueError("out must be (logits, exit_block, token_counts)")
+        _expect(out[0], "logits", (B, info["classes"]), torch.float32, device)
+        _expect(out[1], "exit_block", (B,), torch.int32, device)
+        _expect(out[2], "token_counts", (B, info["layers"]), torch.int32, device)
+    if trace is not None:
+        L, T0 = info["layers"], info["n0"] + 1
+        spec = {"r": ((L, B), torch.int32), "m": ((L, B), torch.float32),
+                "c": ((L, B), torch.float32),
+                "merge_dst": ((L, B, T0), torch.int32),
+                "ids": ((L, B, T0), torch.int32)}
+        for k, (shape, dt) in spec.items():
+            if k not in trace:
+                raise ValueError(f"trace lacks '{k}'")
+            _expect(trace[k], f"trace['{k}']", shape, dt, device)
+    return B
 
 
 class FusionModel:
@@ -41,6 +82,7 @@ class FusionModel:
         check(self._lib.fusion_model_create(blob, len(blob), int(max_batch),
                                             byref(h)))
         self._h = h
+        self.device = torch.device("cuda", torch.cuda.current_device())
         self.info = self.get_info()
 
     def get_info(self) -> dict:
@@ -56,7 +98,7 @@ class FusionModel:
         check(self._lib.fusion_set_router_strength(self._h, c_double(rho)))
 
     def alloc_outputs(self, batch: int):
-        dev = torch.device("cuda")
+        dev = self.device
         logits = torch.empty(batch, self.info["classes"], device=dev)
         exit_block = torch.empty(batch, dtype=torch.int32, device=dev)
         counts = torch.empty(batch, self.info["layers"], dtype=torch.int32, device=dev)
@@ -64,7 +106,7 @@ class FusionModel:
 
     def alloc_trace(self, batch: int) -> dict:
         L, T0 = self.info["layers"], self.info["n0"] + 1
-        dev = torch.device("cuda")
+        dev = self.device
         return dict(r=torch.full((L, batch), -1, dtype=torch.int32, device=dev),
                     m=torch.full((L, batch), -1.0, device=dev),
                     c=torch.full((L, batch), -1.0, device=dev),
@@ -74,8 +116,7 @@ class FusionModel:
     def run(self, images: torch.Tensor, out=None, trace: dict | None = None,
             stream=None):
         """Enqueue a run; returns (logits, exit_block, token_counts)."""
-        _dev_f32(images, "images")
-        B = images.shape[0]
+        B = check_run_args(self.info, self.device, images, out, trace)
         logits, exit_block, counts = out if out is not None else self.alloc_outputs(B)
         sp = _stream_ptr(stream)
         if trace is None:
@@ -93,8 +134,7 @@ class FusionModel:
 
     def debug_state(self, images: torch.Tensor, block: int, stage: int):
         """Packed hidden states after (block, stage); see fusion_debug_state."""
-        _dev_f32(images, "images")
-        B = images.shape[0]
+        B = check_run_args(self.info, self.device, images)
         d, T0 = self.info["d"], self.info["n0"] + 1
         x = torch.zeros(B * T0, d, device="cuda")
         cu = torch.zeros(B + 1, dtype=torch.int32, device="cuda")
