@@ -203,6 +203,120 @@ FUSION_API const char* fusion_profile_kind_name(int k);
 FUSION_API int fusion_profile_read(fusion_model* m, int k, double* total_ms,
                                    int64_t* launches);
 
+/* ------------------------------------------------------------------------
+ * Kernel-level entry points.  Each runs the kernels fusion_run launches for
+ * one step of Algorithm 1 on caller-supplied buffers instead of a model's
+ * workspace, so that the step can be checked (the GPU tests drive every
+ * kernel this way, at random ragged lengths) or used on its own.
+ *
+ * Packed ragged layout: the rows of sample i are rows cu[i] .. cu[i+1]-1 of
+ * every per-row buffer, CLS first; cu is a HOST array of batch + 1 offsets
+ * with cu[0] = 0 and 1 .. 640 rows per sample (M = cu[batch] rows in all);
+ * batch is 1 .. 65536.  Arguments are checked on the host before anything is
+ * enqueued (FUSION_E_INVALID_ARG, nothing launched).  Calls with scratch
+ * (all but fusion_test_gemm) allocate it for the call and synchronise the
+ * stream before returning; fusion_test_gemm is asynchronous.
+ * ------------------------------------------------------------------------ */
+
+/* Ragged token state of a batch (all device pointers but cu). */
+typedef struct fusion_ragged {
+  float* x;               /* device fp32 [M][d] hidden states (row-major) */
+  const float* size;      /* device fp32 [M] token sizes (read only) */
+  const int32_t* origin;  /* device int32 [M] token ids (read only) */
+  const int32_t* cu;      /* HOST int32 [batch + 1] row offsets */
+  int32_t batch;
+  int32_t d;              /* width: a multiple of 32, at most 768 */
+} fusion_ragged;
+
+/* Re-packed state after a step (Sec. III-C: N_b shrinks per sample), all
+ * device buffers owned by the caller:
+ *   rows   int32 [M]          input row of each output row (the fp32 rows
+ *                             themselves are not moved)
+ *   size   fp32  [M]          size of each output row's token
+ *   origin int32 [M]          its id
+ *   cu     int32 [batch + 1]  offsets of the surviving samples (first
+ *                             n_live + 1 entries written)
+ *   live   int32 [batch]      input index of each surviving sample
+ *   counts int32 [2]          n_live, total output rows */
+typedef struct fusion_packed_out {
+  int32_t* rows;
+  float* size;
+  int32_t* origin;
+  int32_t* cu;
+  int32_t* live;
+  int32_t* counts;
+} fusion_packed_out;
+
+/* Epilogues of fusion_test_gemm. */
+enum { FUSION_EPI_STORE = 0, FUSION_EPI_GELU = 1, FUSION_EPI_RESID = 2, FUSION_EPI_F32 = 3 };
+
+/* A token GEMM, the linear maps of Eq. 2 and the heads of Eq. 3 and Eq. 6:
+ * acc[r][n] = sum_k A[r][k] W[n][k] + bias[n] (fp32 accumulation), then
+ *   STORE: out[r][n] = acc (storage type: bf16 rounded to nearest even, or
+ *          fp32);  GELU: out[r][n] = GELU(acc), exact-erf form (storage type);
+ *   RESID: out[p][n] += acc, p = rows ? rows[r] : r (fp32 out);
+ *   F32:   out[p][n]  = acc (fp32 out).
+ * precision 1: A, W bf16 bit patterns (uint16), K % 32 == 0, lda % 8 == 0,
+ * N and ldo multiples of 8 (STORE, GELU) or 4 (RESID, F32); precision 0:
+ * fp32 operands.  A: device [M][lda]; W: device [N][K]; bias: device fp32
+ * [N]; out: device [*][ldo]; rows: device int32 [M] or NULL.  Asynchronous.
+ */
+FUSION_API int fusion_test_gemm(int precision, const void* A, int lda, const void* W, int N,
+                                int K, int M, const float* bias, int epi, void* out,
+                                int ldo, const int32_t* rows, void* stream);
+
+/* Multi-head self-attention of every sample over its own rows (Eq. 2), with
+ * proportional attention when prop_attn = 1 (scores += ln(size of the key
+ * token), the companion of size-weighted merging, Sec. III-C), and the
+ * per-head CLS-attention rows that score tokens for pruning (Eq. 8).
+ * qkv: device [M][3d] in the storage type (columns q | k | v, head-major);
+ * size: device fp32 [M]; out: device [M][d] storage type; cls_scores:
+ * device fp32 [batch][heads][tmax] (row h of sample i: softmax
+ * probabilities of its CLS query, entries past the sample's rows untouched)
+ * or NULL.  precision 1 needs 64-wide heads.  Synchronises the stream. */
+FUSION_API int fusion_test_attention(int precision, const void* qkv, const float* size,
+                                     const int32_t* cu, int batch, int heads, int d,
+                                     int prop_attn, void* out, float* cls_scores, int tmax,
+                                     void* stream);
+
+/* Bipartite soft matching with size-weighted merging (Sec. III-C) of r[i]
+ * token pairs in every sample, then re-compaction: the patch tokens
+ * (rows 1..N) split into A = even and B = odd slots, cosine similarity of
+ * the fp32 rows, best B per A (ties to the lowest B), the r A tokens with
+ * the highest best similarity (ties to the lowest A) merge into their B:
+ * dst = (s_dst x_dst + sum_a s_a x_a) / (s_dst + sum_a s_a), sizes add.
+ * r: HOST int32 [batch], 0 <= r[i] <= floor(N_i / 2).  in->x is updated in
+ * place (each destination row receives its merged value); the survivors,
+ * in order, are described by *out.  merge_dst: device int32
+ * [batch][id_stride] or NULL; entry [i][id of a merged-away token] receives
+ * the id of the token it merged into (origin ids must lie in
+ * 0 .. id_stride-1; others are not recorded).  Synchronises the stream. */
+FUSION_API int fusion_test_merge(const fusion_ragged* in, const int32_t* r, int id_stride,
+                                 int32_t* merge_dst, const fusion_packed_out* out,
+                                 void* stream);
+
+/* Exit check (Eq. 7; optional), top-k pruning of the samples that continue
+ * (Eq. 8) and re-compaction.  Token scores: the head mean of CLS-attention
+ * probabilities, scores = device fp32 [batch][heads][tmax] laid out as
+ * fusion_test_attention writes them; or, when scores is NULL, the learned
+ * linear scorer w . x_t + beta (prune_w: device fp32 [d], prune_b: [1]).
+ * Each continuing sample keeps CLS and the floor(keep_ratio * N) patch
+ * tokens with the highest scores (ties to the lower position), in order.
+ * Exit (exit_logits != NULL): device fp32 [batch][classes] head logits;
+ * c = max softmax; a sample with delta < 1 and c >= delta leaves the batch,
+ * its logits are copied to logits[i] (device fp32 [batch][classes]) and
+ * exit_block[i] (device int32 [batch]) is set to 1.  Optional LayerNorm of
+ * every kept row (eps 1e-6; ln_g, ln_b device fp32 [d]) into ln_out
+ * (device [M][d], row j of the packed output; bf16 for precision 1, else
+ * fp32).  Synchronises the stream. */
+FUSION_API int fusion_test_topk_compact(const fusion_ragged* in, const float* scores, int heads,
+                                        int tmax, const float* prune_w, const float* prune_b,
+                                        double keep_ratio, const float* exit_logits,
+                                        int classes, float delta, float* logits,
+                                        int32_t* exit_block, int precision, const float* ln_g,
+                                        const float* ln_b, void* ln_out,
+                                        const fusion_packed_out* out, void* stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 FUSION_API const char* fusion_last_error(void);
 

@@ -47,6 +47,16 @@ class FusionTrace(ctypes.Structure):
                 ("merge_dst", c_void_p), ("ids", c_void_p)]
 
 
+class FusionRagged(ctypes.Structure):
+    _fields_ = [("x", c_void_p), ("size", c_void_p), ("origin", c_void_p),
+                ("cu", c_void_p), ("batch", c_int32), ("d", c_int32)]
+
+
+class FusionPackedOut(ctypes.Structure):
+    _fields_ = [("rows", c_void_p), ("size", c_void_p), ("origin", c_void_p),
+                ("cu", c_void_p), ("live", c_void_p), ("counts", c_void_p)]
+
+
 class FusionError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"{STATUS.get(code, code)}: {msg}")
@@ -74,6 +84,19 @@ SIGNATURES = [
     ("fusion_profile_kind_name", c_char_p, [c_int]),
     ("fusion_profile_read", c_int, [c_void_p, c_int, POINTER(c_double),
                                     POINTER(c_int64)]),
+    ("fusion_test_gemm", c_int, [c_int, c_void_p, c_int, c_void_p, c_int, c_int,
+                                 c_int, c_void_p, c_int, c_void_p, c_int, c_void_p,
+                                 c_void_p]),
+    ("fusion_test_attention", c_int, [c_int, c_void_p, c_void_p, c_void_p, c_int,
+                                      c_int, c_int, c_int, c_void_p, c_void_p, c_int,
+                                      c_void_p]),
+    ("fusion_test_merge", c_int, [POINTER(FusionRagged), c_void_p, c_int, c_void_p,
+                                  POINTER(FusionPackedOut), c_void_p]),
+    ("fusion_test_topk_compact", c_int, [POINTER(FusionRagged), c_void_p, c_int, c_int,
+                                         c_void_p, c_void_p, c_double, c_void_p, c_int,
+                                         c_float, c_void_p, c_void_p, c_int, c_void_p,
+                                         c_void_p, c_void_p, POINTER(FusionPackedOut),
+                                         c_void_p]),
     ("fusion_last_error", c_char_p, []),
 ]
 

@@ -354,6 +354,13 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   const size_t tr_row = (size_t)(a.b - 1) * a.B + orig;
 
   constexpr int TMAX = Z::TMAX, AMAX = Z::AMAX, BMAX = Z::BMAX, SKP = Z::SKP, SAG = Z::SAG;
+  // the host's token bound selects the size class and is exact; a sample
+  // beyond it (never produced by the library itself) is dropped rather than
+  // overrunning the per-token LDS arrays
+  if (T > TMAX || T < 1) {
+    if (tid == 0) a.newlen[i] = 0;
+    return;
+  }
   __shared__ float sc[TMAX];
   __shared__ float szs[TMAX];
   __shared__ int prow[TMAX];  // physical row of x for each of the sample's tokens
@@ -398,7 +405,10 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
 
   // ---------------------------------------------------------- merge --
   int r = 0;
-  if (a.isM) {
+  if (a.isM && a.r_fixed) {
+    r = min(max(a.r_fixed[i], 0), N / 2);
+    if (tid == 0 && a.tr_r) a.tr_r[tr_row] = r;
+  } else if (a.isM) {
     float z = 0.f;
     const float* xc = a.x + (size_t)prow[0] * d;
     for (int k = tid; k < d; k += AD_NT) z = fmaf(a.router_w[k], xc[k], z);
@@ -512,9 +522,11 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     for (int q = tid; q < r; q += AD_NT) {
       const int aa = clist[q];
       keepf[1 + 2 * aa] = 0;
-      if (a.tr_merge)
-        a.tr_merge[tr_row * (a.n0 + 1) + a.origin[base + 1 + 2 * aa]] =
-            a.origin[base + 2 + 2 * best[aa]];
+      if (a.tr_merge) {
+        const int so = a.origin[base + 1 + 2 * aa];
+        if (so >= 0 && so <= a.n0)
+          a.tr_merge[tr_row * (a.n0 + 1) + so] = a.origin[base + 2 + 2 * best[aa]];
+      }
     }
     __syncthreads();
   }
@@ -605,11 +617,11 @@ hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
   if (a.T_ub <= 128 && a.d % AdSize<128>::SKC == 0) {
     adapt_kernel<AdSize<128>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
-  } else if (a.n0 + 1 <= 256) {
+  } else if (a.T_ub <= 256) {
     if (a.d % AdSize<256>::SKC != 0) return hipErrorInvalidValue;
     adapt_kernel<AdSize<256>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
   } else {
-    if (a.n0 + 1 > AD_TMAX || a.d % AdSize<AD_TMAX>::SKC != 0) return hipErrorInvalidValue;
+    if (a.T_ub > AD_TMAX || a.d % AdSize<AD_TMAX>::SKC != 0) return hipErrorInvalidValue;
     adapt_kernel<AdSize<AD_TMAX>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
   }
   return hipGetLastError();
@@ -656,6 +668,7 @@ __global__ __launch_bounds__(256) void compact_kernel(CompactArgs a) {
   }
   if (i >= nl || a.newlen[i] == 0) return;
   const int base = a.cu[i], Tn = a.cu[i + 1] - base;
+  if (Tn > AD_TMAX) return;  // never kept by the adapt kernel (newlen 0)
   const int orig = a.live[i];
   if (tid == 0 && part == 0) {
     a.cu2[j] = off;

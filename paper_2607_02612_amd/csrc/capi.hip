@@ -254,6 +254,8 @@ const char* kKindNames[K_COUNT] = {
 
 }  // namespace
 
+int fusion::api_fail(int code, const char* msg) { return fail(code, msg); }
+
 struct BlockW {
   const float *ln1_g, *ln1_b, *qkv_b, *proj_b, *ln2_g, *ln2_b, *fc1_b, *fc2_b;
   const void *qkv_w, *proj_w, *fc1_w, *fc2_w;

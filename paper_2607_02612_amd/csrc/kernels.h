@@ -102,6 +102,7 @@ struct AdaptArgs {
   const float* prune_b;  // [1]
   const float* router_w;
   const float* router_b;
+  const int* r_fixed;  // optional [nlive]: merge counts given by the caller (no router)
   int r_b;
   double rho;
   const float* head_buf;  // [nlive, C] exit-head logits
@@ -149,6 +150,14 @@ struct CompactArgs {
 };
 template <typename T>
 hipError_t launch_compact(const CompactArgs& a, hipStream_t s);
+
+// Scratch of the kernel-level entry points: live map and row map set to the
+// identity, live counts (nlive = B, M rows).
+hipError_t launch_step_init(int* live, int B, int* rmap, int M, LiveCounts* cnt,
+                            hipStream_t s);
+
+// Error channel of the C ABI (message returned by fusion_last_error).
+int api_fail(int code, const char* msg);
 
 // Copy of the packed state for diagnostics.
 hipError_t launch_copy_state(const float* x, const int* rmap, const int* cu, const int* live,

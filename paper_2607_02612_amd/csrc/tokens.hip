@@ -201,6 +201,29 @@ template hipError_t launch_pool_ln<bf16_t>(const float*, const int*, const float
                                            const LiveCounts*, const float*, const float*,
                                            bf16_t*, int, int, hipStream_t);
 
+__global__ void step_init_kernel(int* __restrict__ live, int B, int* __restrict__ rmap, int M,
+                                 LiveCounts* cnt) {
+  const int n = B > M ? B : M;
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < n; t += gridDim.x * blockDim.x) {
+    if (t < B) live[t] = t;
+    if (t < M) rmap[t] = t;
+    if (t == 0) {
+      cnt->nlive = B;
+      cnt->M = M;
+    }
+  }
+}
+
+hipError_t launch_step_init(int* live, int B, int* rmap, int M, LiveCounts* cnt,
+                            hipStream_t s) {
+  const int n = B > M ? B : M;
+  int blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  step_init_kernel<<<blocks, 256, 0, s>>>(live, B, rmap, M, cnt);
+  return hipGetLastError();
+}
+
 __global__ void copy_state_kernel(const float* __restrict__ x, const int* rmap, const int* cu,
                                   const int* live, const LiveCounts* cnt,
                                   float* __restrict__ x_out, int* cu_out,

@@ -137,3 +137,59 @@ def test_blob_inspect_reads_paper_rules():
         bad = bytearray(b)
         bad[off:off + 4] = struct.pack("<I", 5)
         assert "rule" in _expect(-2, bytes(bad))
+
+
+def _ragged_args(cu, d=64):
+    cu = np.asarray(cu, dtype=np.int32)
+    rg = _native.FusionRagged(8, 8, 8, cu.ctypes.data_as(ctypes.c_void_p), len(cu) - 1, d)
+    po = _native.FusionPackedOut(8, 8, 8, 8, 8, 8)
+    return cu, rg, po
+
+
+@pytest.mark.parametrize("cu,r,d", [
+    ([1, 5], [0], 64),            # offsets must start at 0
+    ([0, 0], [0], 64),            # empty sample
+    ([0, 641], [0], 64),          # more than 640 rows
+    ([0, 5, 3], [0, 0], 64),      # decreasing offsets
+    ([0, 5], [3], 64),            # r > floor(N/2)
+    ([0, 5], [-1], 64),           # negative r
+    ([0, 5], [1], 48),            # width not a multiple of 32
+    ([0, 5], [1], 800),           # width beyond 768
+])
+def test_kernel_level_merge_rejects_bad_arguments_on_host(cu, r, d):
+    """fusion_test_merge validates offsets, counts and width before any
+    device call (the pointers here are never dereferenced)."""
+    lib = _native.lib()
+    cu, rg, po = _ragged_args(cu, d)
+    r = np.asarray(r, dtype=np.int32)
+    rc = lib.fusion_test_merge(ctypes.byref(rg), r.ctypes.data_as(ctypes.c_void_p), 8, None,
+                               ctypes.byref(po), None)
+    assert rc == -1, lib.fusion_last_error()
+    assert lib.fusion_last_error().decode() != ""
+
+
+def test_kernel_level_entry_points_reject_bad_arguments_on_host():
+    lib = _native.lib()
+    # GEMM: unknown precision / epilogue, bf16 K not a multiple of 32, row
+    # map with a bf16 store epilogue
+    assert lib.fusion_test_gemm(2, 8, 64, 8, 64, 64, 4, 8, 0, 8, 64, None, None) == -1
+    assert lib.fusion_test_gemm(1, 8, 64, 8, 64, 64, 4, 8, 7, 8, 64, None, None) == -1
+    assert lib.fusion_test_gemm(1, 8, 48, 8, 64, 48, 4, 8, 0, 8, 64, None, None) == -1
+    assert lib.fusion_test_gemm(1, 8, 64, 8, 64, 64, 4, 8, 0, 8, 64, 8, None) == -1
+    assert lib.fusion_test_gemm(1, None, 64, 8, 64, 64, 4, 8, 0, 8, 64, None, None) == -1
+    # attention: bf16 needs 64-wide heads; tmax below the longest sample
+    cu = np.array([0, 3, 10], dtype=np.int32)
+    cp = cu.ctypes.data_as(ctypes.c_void_p)
+    assert lib.fusion_test_attention(1, 8, 8, cp, 2, 4, 128, 1, 8, None, 0, None) == -1
+    assert lib.fusion_test_attention(1, 8, 8, cp, 2, 2, 128, 1, 8, 8, 5, None) == -1
+    # top-k: no score source, keep ratio outside [0, 1], exit without outputs
+    cu, rg, po = _ragged_args([0, 4, 9])
+    br = ctypes.byref
+    assert lib.fusion_test_topk_compact(br(rg), None, 1, 9, None, None, 0.5, None, 0, 1.0,
+                                        None, None, 1, None, None, None, br(po), None) == -1
+    assert lib.fusion_test_topk_compact(br(rg), 8, 1, 9, None, None, 1.5, None, 0, 1.0,
+                                        None, None, 1, None, None, None, br(po), None) == -1
+    assert lib.fusion_test_topk_compact(br(rg), 8, 1, 9, None, None, 0.5, 8, 10, 0.5,
+                                        None, None, 1, None, None, None, br(po), None) == -1
+    assert lib.fusion_test_topk_compact(br(rg), 8, 1, 4, None, None, 0.5, None, 0, 1.0,
+                                        None, None, 1, None, None, None, br(po), None) == -1

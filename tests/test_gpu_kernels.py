@@ -1,0 +1,344 @@
+"""Kernel-level GPU parity through the C ABI's fusion_test_* entry points:
+each kernel of the pipeline runs on caller-supplied packed ragged buffers
+and is compared with the oracle's function for that step, at random ragged
+lengths that include the degenerate cases (T = 1, T = 2, odd N, r = 0,
+r = floor(N/2), k = 0, k = N, every sample exiting).
+
+Merge and learned-score prune decisions follow the oracle's near-tie rule
+(the GPU's choice may differ only where the oracle's margin is below 1e-3;
+any other difference fails); CLS-attention prune scores are bit-identical
+on both sides, so those decisions must match exactly.
+"""
+import numpy as np
+import pytest
+
+from oracle import fusion_oracle as fo
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _kern():
+    from paper_2607_02612_amd import kernels
+    return kernels
+
+
+def _bf16(rng, shape, scale=1.0):
+    return fo.bf16_round((rng.standard_normal(shape) * scale).astype(np.float32))
+
+
+def _to_dev_bf16(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda().to(torch.bfloat16)
+
+
+def _offsets(lengths):
+    return np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+
+
+# ------------------------------------------------------------------ GEMM --
+GEMM_SHAPES = [(1, 1152, 384), (37, 1152, 384), (300, 1536, 384), (1000, 384, 1536),
+               (129, 384, 384), (70, 1000, 384), (2049, 384, 384)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("epi", ["store", "gelu", "resid", "f32"])
+def test_gemm_bf16(torch_cuda, M, N, K, epi):
+    torch = torch_cuda
+    if epi in ("store", "gelu") and N % 8:
+        pytest.skip("bf16 outputs need N % 8 == 0")
+    print(f"[gemm bf16] M={M} N={N} K={K} epi={epi}", flush=True)
+    rng = np.random.default_rng(M * 7 + N + K)
+    A, W = _bf16(rng, (M, K)), _bf16(rng, (N, K), 0.05)
+    bias = rng.standard_normal(N).astype(np.float32) * 0.1
+    ref = A.astype(np.float64) @ W.astype(np.float64).T + bias
+    bound = np.abs(A).astype(np.float64) @ np.abs(W).astype(np.float64).T
+    dA, dW = _to_dev_bf16(torch, A), _to_dev_bf16(torch, W)
+    db = torch.from_numpy(bias).cuda()
+    k = _kern()
+    if epi in ("store", "gelu"):
+        out = torch.zeros(M, N, dtype=torch.bfloat16, device="cuda")
+        k.gemm(dA, dW, db, epi, out)
+        g = out.float().cpu().numpy()
+        pre = ref.astype(np.float32)
+        r = fo.gelu(pre) if epi == "gelu" else pre
+        # one bf16 rounding of a value that differs only by the fp32
+        # accumulation order (and, for GELU, the 7e-7 approximation)
+        err = np.abs(g - r) - (2.0 ** -8 * np.abs(r) + 1e-5 * bound + 1e-6)
+        assert (err <= 0).all(), float(err.max())
+        return
+    rows = None
+    nrow = M
+    if epi in ("resid", "f32"):
+        nrow = M + 5
+        perm = rng.permutation(nrow)[:M].astype(np.int32)
+        rows = torch.from_numpy(perm).cuda()
+    x0 = rng.standard_normal((nrow, N)).astype(np.float32)
+    out = torch.from_numpy(x0.copy()).cuda()
+    k.gemm(dA, dW, db, epi, out, rows=rows)
+    g = out.cpu().numpy()
+    want = x0.astype(np.float64).copy()
+    idx = perm
+    want[idx] = (want[idx] if epi == "resid" else 0.0) + ref
+    tol = 1e-5 * (bound + np.abs(x0[idx])) + 1e-6
+    assert np.all(np.abs(g[idx] - want[idx]) <= tol)
+    untouched = np.setdiff1d(np.arange(nrow), idx)
+    assert np.array_equal(g[untouched], x0[untouched])
+
+
+@pytest.mark.parametrize("M,N,K,epi", [(1, 64, 64, "store"), (65, 256, 64, "gelu"),
+                                       (130, 64, 256, "resid"), (9, 10, 64, "f32")])
+def test_gemm_fp32(torch_cuda, M, N, K, epi):
+    torch = torch_cuda
+    rng = np.random.default_rng(N + K + M)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.standard_normal((N, K)) * 0.1).astype(np.float32)
+    bias = rng.standard_normal(N).astype(np.float32)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T + bias
+    x0 = rng.standard_normal((M, N)).astype(np.float32)
+    out = torch.from_numpy(x0.copy()).cuda()
+    _kern().gemm(torch.from_numpy(A).cuda(), torch.from_numpy(W).cuda(),
+                 torch.from_numpy(bias).cuda(), epi, out)
+    g = out.cpu().numpy()
+    want = {"store": ref, "gelu": fo.gelu(ref.astype(np.float32)), "resid": x0 + ref,
+            "f32": ref}[epi]
+    assert np.abs(g - want).max() <= 1e-4
+
+
+# ------------------------------------------------------------- attention --
+ATT_CASES = [
+    # lengths, heads, dh, precision, prop_attn
+    ([1, 2, 17, 64, 197, 250, 33], 6, 64, "bf16", True),
+    ([1, 2, 17, 64, 197, 250, 33], 6, 64, "bf16", False),
+    ([577, 1, 300, 129, 2, 400], 6, 64, "bf16", True),
+    ([1, 2, 33, 65, 7], 2, 32, "fp32", True),
+]
+
+
+@pytest.mark.parametrize("lengths,H,dh,prec,prop", ATT_CASES)
+def test_attention_ragged(torch_cuda, lengths, H, dh, prec, prop):
+    torch = torch_cuda
+    print(f"[attention] T={lengths} H={H} {prec} prop={prop}", flush=True)
+    rng = np.random.default_rng(sum(lengths) + H)
+    cu = _offsets(lengths)
+    M, d = int(cu[-1]), H * dh
+    mode = "bf16emu" if prec == "bf16" else "fp32"
+    qkv = fo._rnd((rng.standard_normal((M, 3 * d)) * 1.2).astype(np.float32), mode)
+    size = rng.integers(1, 5, size=M).astype(np.float32) if prop else np.ones(M, np.float32)
+    tmax = max(lengths) + 3
+    dq = _to_dev_bf16(torch, qkv) if prec == "bf16" else torch.from_numpy(qkv).cuda()
+    out, cls = _kern().attention(dq, torch.from_numpy(size).cuda(), cu, H, prop, cls_tmax=tmax)
+    O = out.float().cpu().numpy()
+    C = cls.cpu().numpy()
+    worst = 0.0
+    for i, T in enumerate(lengths):
+        a, b = cu[i], cu[i + 1]
+        Oref, cref = fo.attention_heads(qkv[a:b], size[a:b], H, int(prop), mode, True)
+        e = np.abs(O[a:b] - Oref)
+        if prec == "bf16":
+            # exp in base 2 with folded constants and one bf16 rounding of E
+            # and of O on each side
+            assert (e <= 1e-2 + 2.0 ** -7 * np.abs(Oref)).all(), (i, T, float(e.max()))
+        else:
+            assert e.max() <= 1e-5, (i, T, float(e.max()))
+        worst = max(worst, float(e.max()))
+        cmean = C[i, :, :T].mean(axis=0)
+        assert np.abs(cmean - cref).max() <= 2e-6, (i, T)
+        assert np.all(C[i, :, T:] == -1.0), "entries past the sample untouched"
+        assert np.abs(C[i, :, :T].sum(axis=1) - 1.0).max() <= 1e-5
+    print(f"  max |dO| = {worst:.3e}")
+
+
+# ----------------------------------------------------------------- merge --
+def _tokens(rng, T, d, rank=8):
+    """Hidden states with a low-rank structure (cosines spread over [-1, 1])."""
+    basis = rng.standard_normal((rank, d))
+    c = rng.standard_normal((T, rank))
+    return (c @ basis + 0.4 * rng.standard_normal((T, d))).astype(np.float32)
+
+
+MERGE_CASES = [
+    # lengths, d
+    ([1, 2, 3, 4, 17, 64, 97, 128], 384),     # size class T <= 128
+    ([1, 2, 3, 18, 129, 197, 256, 65], 384),  # T <= 256
+    ([577, 300, 1, 2, 451], 384),             # T <= 640
+    ([197, 5, 66, 31], 192),
+]
+
+
+@pytest.mark.parametrize("lengths,d", MERGE_CASES)
+def test_merge_ragged(torch_cuda, lengths, d):
+    torch = torch_cuda
+    print(f"[merge] T={lengths} d={d}", flush=True)
+    rng = np.random.default_rng(len(lengths) * 1000 + d + lengths[0])
+    cu = _offsets(lengths)
+    M = int(cu[-1])
+    x = np.concatenate([_tokens(rng, T, d) for T in lengths])
+    size = rng.integers(1, 4, size=M).astype(np.float32)
+    id_stride = max(lengths) + 7
+    origin = np.concatenate([np.sort(rng.permutation(id_stride)[:T]) for T in lengths]).astype(np.int32)
+    r = []
+    for j, T in enumerate(lengths):
+        N = T - 1
+        r.append([0, N // 2, N // 2, rng.integers(0, N // 2 + 1)][j % 4])
+    r = np.array(r, dtype=np.int32)
+    dx = torch.from_numpy(x.copy()).cuda()
+    o, md = _kern().merge(dx, torch.from_numpy(size).cuda(), torch.from_numpy(origin).cuda(),
+                          cu, r, id_stride)
+    torch.cuda.synchronize()
+    xg = dx.cpu().numpy()
+    o = {k: v.cpu().numpy() for k, v in o.items()}
+    md = md.cpu().numpy()
+    B = len(lengths)
+    assert list(o["counts"]) == [B, int(M - r.sum())]
+    assert list(o["live"]) == list(range(B))
+    assert np.array_equal(o["cu"], _offsets([T - int(rr) for T, rr in zip(lengths, r)]))
+    adopted = []
+    for i, T in enumerate(lengths):
+        a, b = cu[i], cu[i + 1]
+        xs, ss, og = x[a:b], size[a:b], origin[a:b].astype(np.int64)
+        plan = fo.merge_plan(xs, int(r[i]))
+        gmap = {int(s_): int(t_) for s_, t_ in enumerate(md[i]) if t_ >= 0}
+        chosen, dst = fo._follow_merge(1, plan, int(r[i]), og, gmap, fo.TOL, adopted)
+        if r[i] > 0:
+            xr, sr, _, orr = fo.apply_merge(xs, ss, None, og, plan["A"], plan["B"], chosen, dst)
+        else:
+            xr, sr, orr = xs, ss, og
+        p, q = o["cu"][i], o["cu"][i + 1]
+        assert np.array_equal(o["origin"][p:q], orr), i
+        assert np.array_equal(o["size"][p:q], sr), i
+        rows = o["rows"][p:q]
+        assert np.all((rows >= a) & (rows < b))
+        got = xg[rows]
+        assert np.abs(got - xr).max() <= 2e-6 * max(1.0, float(np.abs(xr).max())), i
+    n_dec = int(r.sum())
+    print(f"  merges={n_dec} near-tie adoptions={len(adopted)}")
+    assert len(adopted) <= max(2, n_dec // 20)
+
+
+# --------------------------------------------------------- prune, compact --
+def _cls_scores(rng, lengths, H, tmax):
+    S = np.full((len(lengths), H, tmax), -3.0, dtype=np.float32)
+    for i, T in enumerate(lengths):
+        e = rng.random((H, T)).astype(np.float32) ** 3 + 1e-3
+        S[i, :, :T] = e / e.sum(axis=1, keepdims=True)
+    return S
+
+
+@pytest.mark.parametrize("keep,rho", [(0.7, 1.0), (0.7, 1.5), (0.0, 1.0), (1.0, 1.0)])
+def test_topk_compact_cls_attention(torch_cuda, keep, rho):
+    torch = torch_cuda
+    lengths = [1, 2, 3, 10, 65, 197, 128, 300, 4]
+    print(f"[topk cls] tau={keep} rho={rho}", flush=True)
+    rng = np.random.default_rng(int(keep * 100 + rho * 10))
+    H, d = 6, 384
+    cu = _offsets(lengths)
+    M, B = int(cu[-1]), len(lengths)
+    x = np.concatenate([_tokens(rng, T, d) for T in lengths])
+    size = rng.integers(1, 4, size=M).astype(np.float32)
+    origin = np.concatenate([np.arange(T) for T in lengths]).astype(np.int32)
+    tmax = max(lengths)
+    S = _cls_scores(rng, lengths, H, tmax)
+    C = 10
+    lg = rng.standard_normal((B, C)).astype(np.float32)
+    lg[::3, 2] += 6.0                                  # confident: exits
+    delta = 0.5
+    g = (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+    bb = (0.1 * rng.standard_normal(d)).astype(np.float32)
+    tau_eff = min(1.0, max(0.0, 1.0 - rho * (1.0 - keep)))
+    T_ = torch.from_numpy
+    o, logits, eb, ln_out = _kern().topk_compact(
+        T_(x).cuda(), T_(size).cuda(), T_(origin).cuda(), cu, tau_eff, scores=T_(S).cuda(),
+        heads=H, exit_logits=T_(lg).cuda(), delta=delta, ln=(T_(g).cuda(), T_(bb).cuda()))
+    o = {k: v.cpu().numpy() for k, v in o.items()}
+    logits, eb, ln_out = logits.cpu().numpy(), eb.cpu().numpy(), ln_out.float().cpu().numpy()
+    j = 0
+    for i, T in enumerate(lengths):
+        c = fo.max_softmax(lg[i])
+        assert abs(float(c) - delta) > 1e-4
+        if c >= delta:
+            assert eb[i] == 1 and np.array_equal(logits[i], lg[i])
+            assert i not in o["live"][:o["counts"][0]]
+            continue
+        assert eb[i] == -1 and np.all(logits[i] == -7.0)
+        assert o["live"][j] == i
+        a = cu[i]
+        acc = S[i, 0, :T].copy()
+        for h in range(1, H):
+            acc = acc + S[i, h, :T]
+        score = (acc / np.float32(H)).astype(np.float32)
+        k = fo.keep_count(T - 1, keep, rho)
+        kept, _, _ = fo.prune_plan(score, k)
+        rows = np.concatenate([[0], 1 + kept])
+        p, q = o["cu"][j], o["cu"][j + 1]
+        assert q - p == k + 1
+        assert np.array_equal(o["origin"][p:q], origin[a + rows])
+        assert np.array_equal(o["rows"][p:q], a + rows)
+        assert np.array_equal(o["size"][p:q], size[a + rows])
+        ref = fo.bf16_round(fo.layer_norm(x[a + rows], g, bb))
+        assert np.abs(ln_out[p:q] - ref).max() <= 2.0 ** -7 * max(1.0, float(np.abs(ref).max()))
+        j += 1
+    assert o["counts"][0] == j
+    assert o["counts"][1] == o["cu"][j]
+
+
+def test_topk_compact_learned_scorer_fp32_ln(torch_cuda):
+    torch = torch_cuda
+    lengths = [1, 2, 9, 64, 197, 5]
+    rng = np.random.default_rng(11)
+    d = 256
+    cu = _offsets(lengths)
+    M = int(cu[-1])
+    x = np.concatenate([_tokens(rng, T, d) for T in lengths])
+    size = np.ones(M, np.float32)
+    origin = np.concatenate([np.arange(T) for T in lengths]).astype(np.int32)
+    w = (rng.standard_normal(d) / np.sqrt(d)).astype(np.float32)
+    beta = np.array([0.3], np.float32)
+    g = np.ones(d, np.float32)
+    bb = np.zeros(d, np.float32)
+    T_ = torch.from_numpy
+    o, _, _, ln_out = _kern().topk_compact(
+        T_(x).cuda(), T_(size).cuda(), T_(origin).cuda(), cu, 0.7, prune_w=T_(w).cuda(),
+        prune_b=T_(beta).cuda(), ln=(T_(g).cuda(), T_(bb).cuda()), precision=0)
+    o = {k: v.cpu().numpy() for k, v in o.items()}
+    ln_out = ln_out.cpu().numpy()
+    assert list(o["counts"]) == [len(lengths), int(sum(1 + int(np.floor(0.7 * (T - 1))) for T in lengths))]
+    adopted = []
+    for i, T in enumerate(lengths):
+        a = cu[i]
+        score = fo.learned_scores(x[a:a + T], w, beta[0])
+        k = fo.keep_count(T - 1, 0.7, 1.0)
+        kept, _, order = fo.prune_plan(score, k, 1.0)
+        p, q = o["cu"][i], o["cu"][i + 1]
+        kept = fo._follow_prune(1, score, k, kept, order, origin[a:a + T].astype(np.int64),
+                                list(o["origin"][p:q]), fo.TOL, adopted, 1.0)
+        rows = np.concatenate([[0], 1 + kept])
+        assert np.array_equal(o["rows"][p:q], a + rows)
+        ref = fo.layer_norm(x[a + rows], g, bb)
+        assert np.abs(ln_out[p:q] - ref).max() <= 1e-5
+    assert len(adopted) <= 1
+
+
+def test_topk_compact_every_sample_exits(torch_cuda):
+    torch = torch_cuda
+    lengths = [3, 1, 20]
+    rng = np.random.default_rng(5)
+    cu = _offsets(lengths)
+    M, B = int(cu[-1]), len(lengths)
+    x = rng.standard_normal((M, 64)).astype(np.float32)
+    S = _cls_scores(rng, lengths, 2, 20)
+    lg = rng.standard_normal((B, 4)).astype(np.float32)
+    T_ = torch.from_numpy
+    o, logits, eb, _ = _kern().topk_compact(
+        T_(x).cuda(), T_(np.ones(M, np.float32)).cuda(),
+        T_(np.zeros(M, np.int32)).cuda(), cu, 0.7, scores=T_(S).cuda(), heads=2,
+        exit_logits=T_(lg).cuda(), delta=0.0)
+    assert list(o["counts"].cpu().numpy()) == [0, 0]
+    assert np.all(eb.cpu().numpy() == 1)
+    assert np.array_equal(logits.cpu().numpy(), lg)
