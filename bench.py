@@ -288,6 +288,11 @@ class EnergyMeter:
         return out
 
 
+def progress(msg):
+    """A progress line on stderr (the JSON line alone goes to stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def run_timed(model, x, out, steps, warmup, delta=None, rho=None):
     """Warm up, then time `steps` runs on the current stream with HIP events;
     returns ms per step and the last run's outputs (host)."""
@@ -352,26 +357,63 @@ def paper_section(args, energy):
         r = summarize(cfg_of[st["model"]], B, ms, eb, cnt)
         r.update(delta=None if st["delta"] is None else list(st["delta"]), rho=st["rho"])
         res[name] = r
+        progress(f"paper setting {name}: {r['images_per_s']:.0f} images/s")
     for name in res:
         res[name]["speedup_vs_plain"] = res["plain"]["ms_per_step"] / res[name]["ms_per_step"]
-    # energy: a region of about two seconds per setting
-    for name, st in settings.items():
-        mdl = models[st["model"]]
-        ob = mdl.alloc_outputs(B)
-        n = max(1, int(2000.0 / res[name]["ms_per_step"]))
+    # energy: regions of about args.energy_seconds per setting, the settings
+    # interleaved and the round repeated args.energy_reps times, so that
+    # drifts of the board's power management fall on every setting alike;
+    # mean and spread (min, max) per setting
+    e_names = ["plain", "balanced", "power_save"]
+    regions = {name: [] for name in e_names}
+    for rep in range(args.energy_reps):
+        for name in e_names:
+            st = settings[name]
+            mdl = models[st["model"]]
+            ob = mdl.alloc_outputs(B)
+            if st["delta"] is not None:
+                mdl.set_exit_thresholds(list(st["delta"]))
+            if st["rho"] is not None:
+                mdl.set_router_strength(st["rho"])
+            n = max(1, int(1e3 * args.energy_seconds / res[name]["ms_per_step"]))
 
-        def loop():
-            for _ in range(n):
-                mdl.run(x, out=ob)
-            torch.cuda.synchronize()
-        e = energy.measure(loop)
-        if "joules_counter" in e:
-            e["mj_per_image_counter"] = 1e3 * e["joules_counter"] / (n * B)
-        if "joules_sampled" in e:
-            e["mj_per_image_sampled"] = 1e3 * e["joules_sampled"] / (n * B)
-        e["images"] = n * B
-        e["images_per_s_in_region"] = n * B / e["seconds"] if "seconds" in e else None
-        res[name]["energy"] = e
+            def loop():
+                for _ in range(n):
+                    mdl.run(x, out=ob)
+                torch.cuda.synchronize()
+            e = energy.measure(loop)
+            if "joules_counter" in e:
+                e["mj_per_image_counter"] = 1e3 * e["joules_counter"] / (n * B)
+            if "joules_sampled" in e:
+                e["mj_per_image_sampled"] = 1e3 * e["joules_sampled"] / (n * B)
+            e["images"] = n * B
+            e["images_per_s_in_region"] = n * B / e["seconds"] if "seconds" in e else None
+            regions[name].append(e)
+            progress(f"energy region {rep + 1}/{args.energy_reps} {name}: "
+                     f"{e.get('mj_per_image_counter', float('nan')):.2f} mJ/image")
+    for name in e_names:
+        rs = regions[name]
+        summ = {"regions": rs, "seconds_per_region": args.energy_seconds}
+        for key in ("mj_per_image_counter", "mj_per_image_sampled", "images_per_s_in_region",
+                    "mean_power_w"):
+            v = [r[key] for r in rs if isinstance(r.get(key), (int, float))]
+            if v:
+                summ[key] = {"mean": float(np.mean(v)), "min": float(np.min(v)),
+                             "max": float(np.max(v))}
+        res[name]["energy"] = summ
+    # a difference in energy per image is claimed only where the ranges of
+    # the repeated regions do not overlap
+    cmp = {}
+    base = res["plain"]["energy"].get("mj_per_image_counter")
+    for name in ("balanced", "power_save"):
+        v = res[name]["energy"].get("mj_per_image_counter")
+        if base and v:
+            separated = v["max"] < base["min"] or v["min"] > base["max"]
+            cmp[name] = {"saving_vs_plain": 1.0 - v["mean"] / base["mean"],
+                         "ranges_separated": bool(separated)}
+    energy_summary = {"method": "GPU energy accumulator (amd-smi) over each region; "
+                                "settings interleaved, repeated; mean (min, max)",
+                      "vs_plain": cmp}
     # batch sweep (Fig. 6 protocol: throughput and latency against batch)
     sweep = {}
     for b in (1, 8, 32, 64, 128, 256):
@@ -383,28 +425,16 @@ def paper_section(args, energy):
         for name in row:
             row[name]["speedup_vs_plain"] = row["plain"]["ms_per_step"] / row[name]["ms_per_step"]
         sweep[str(b)] = row
+        progress(f"batch sweep {b} done")
     for mdl in models.values():
         mdl.close()
-    return {"workload": f"deit_s_paper batch {B}: merge (fraction rule) at "
+    return {"energy": energy_summary,
+            "workload": f"deit_s_paper batch {B}: merge (fraction rule) at "
                         f"{list(cfg['merges'])}, exit heads {list(cfg['exits'])} "
                         f"({', '.join(cfg['exit_kind'])}, hidden {cfg['exit_hidden']}), "
                         f"learned prune keep {cfg['tau']} at {list(cfg['prunes'])}",
             "dense_gflop_per_image": dense_flops(cfg) / 1e9,
             "profiles": res, "batch_sweep": sweep}
-
-
-ABLATION = [
-    # name, layer-set overrides (Tab. VII rows), profile
-    ("plain", dict(merges=(), exits=(), prunes=()), "balanced"),
-    ("pruning only", dict(merges=(), exits=()), "balanced"),
-    ("merging only", dict(exits=(), prunes=()), "balanced"),
-    ("early exit only", dict(merges=(), prunes=()), "balanced"),
-    ("parallel prune + exit", dict(merges=(), prunes=(3, 6, 9)), "balanced"),
-    ("sequential exit -> prune", dict(merges=()), "balanced"),
-    ("full sequential, fixed r=8 merges", dict(merge_rule="budget", r=8), "balanced"),
-    ("full sequential, merge routers", dict(), "balanced"),
-    ("full sequential, routers + power_save scaling", dict(), "power_save"),
-]
 
 
 def ablation_section(args):
@@ -413,17 +443,14 @@ def ablation_section(args):
     import torch
     from paper_2607_02612_amd import FusionModel
     from synth import blob, configs, images, weights
-    sup = configs.get("deit_s_paper", prunes=(3, 6, 9, 10))
+    sup = configs.get("deit_s_paper", prunes=configs.ABLATION_SUPERSET_PRUNES)
     W = weights.make_weights(sup)
     imgs = images.make_images(sup)
     B = sup["batch"]
     x = torch.from_numpy(imgs).cuda()
     rows = {}
-    for name, over, prof in ABLATION:
-        o = dict(over)
-        if "exits" in o and not o["exits"]:
-            o.update(exit_kind=(), delta=())
-        cfg = configs.get("deit_s_paper", **o)
+    for name, over, prof in configs.ABLATION:
+        cfg = configs.ablation_config("deit_s_paper", over)
         if cfg["merge_rule"] == "budget":
             Wc = weights.zero_routers(cfg, W)       # m = 1/2: r = r_b
         else:
@@ -462,6 +489,10 @@ def main():
                     help="headline from replays of the step captured as one HIP "
                          "graph (default: kernel-by-kernel launches; the other "
                          "mode is timed too and reported under 'timing')")
+    ap.add_argument("--energy-seconds", type=float, default=10.0,
+                    help="length of each energy region (the paper section)")
+    ap.add_argument("--energy-reps", type=int, default=3,
+                    help="interleaved repetitions of the energy regions")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 256 MiB device-to-device copy, whose HBM "
                          "counters calibrate FETCH_SIZE / WRITE_SIZE")
@@ -542,6 +573,7 @@ def main():
         if args.headline_only and e_rate != 0.0:
             continue
         sweep[e_rate] = timed(th[e_rate], args.graph)
+        progress(f"exit setting {int(100 * e_rate)}%: {sweep[e_rate]['img_s']:.0f} images/s")
     head = sweep[0.0]
     other = timed(th[0.0], not args.graph)
 
@@ -553,6 +585,7 @@ def main():
     torch.cuda.synchronize()
     prof = model.profile_read()
     model.profile_enable(False)
+    progress("per-kernel event pass done")
     work = kernel_work(cfg, head["counts"])
     kernels = {}
     for k, (ms_tot, n) in prof.items():
@@ -574,17 +607,23 @@ def main():
     dom = max((k for k in kernels if "roofline_bound" in kernels[k]),
               key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
-    if dk["roofline_bound"] == "mfma":
+    wk = work[dom]
+    n_launch = max(1.0, dk["launches_per_step"])
+    if "tflops" in dk:
+        # a dense contraction (the token GEMMs, attention): on the MFMA roof,
+        # with its HBM fraction on algorithmic bytes beside it
         roofline = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                     "peak": BF16_PEAK / 1e12, "unit": "TFLOP/s",
-                    "frac": dk["frac_bf16_peak"], "traffic": measured_traffic(dom)}
+                    "frac": dk["frac_bf16_peak"], "traffic": measured_traffic(dom),
+                    "hbm_gbps": dk["gbps"], "frac_hbm_peak": dk["frac_hbm_peak"],
+                    "roof_binding_at_peaks": dk["roofline_bound"]}
     else:
         roofline = {"kernel": dom, "bound": "hbm", "achieved": dk["gbps"],
                     "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                     "frac": dk["frac_hbm_peak"], "traffic": measured_traffic(dom)}
-    if "tflops" in dk:
-        roofline["mfma_tflops"] = dk["tflops"]
-        roofline["frac_bf16_peak"] = dk["frac_bf16_peak"]
+    roofline["algorithmic_flop_per_launch"] = wk["flop"] / n_launch
+    roofline["algorithmic_bytes_per_launch"] = wk["byte"] / n_launch
+    roofline["mean_launch_us"] = dk["ms_per_step"] / n_launch * 1e3
     # the whole step on the roofline: executed FLOPs at the MFMA peak against
     # the algorithmic bytes of all kinds at the HBM peak
     step_bytes = sum(w["byte"] for w in work.values())
@@ -633,15 +672,17 @@ def main():
             roofline["frac_of_measured"] = roofline["achieved"] / mp["hbm_copy_gbps"]
         else:
             roofline["frac_of_measured"] = roofline["achieved"] / mp["bf16_gemm_tflops"]
-        if "mfma_tflops" in roofline:
-            roofline["frac_of_measured_gemm"] = roofline["mfma_tflops"] / mp["bf16_gemm_tflops"]
+        if roofline["unit"] == "TFLOP/s":
+            roofline["hbm_frac_of_measured_copy"] = roofline["hbm_gbps"] / mp["hbm_copy_gbps"]
         line["pct_measured_gemm_peak_executed"] = (
             100.0 * head["flops"] / (head["ms"] / 1e3) / (mp["bf16_gemm_tflops"] * 1e12))
     if not (args.no_paper or args.headline_only):
         model.close()
         energy = EnergyMeter()
         line["paper"] = paper_section(args, energy)
+        progress("paper section done")
         line["ablation"] = ablation_section(args)
+        progress("ablation section done")
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(cfg, W, imgs, args.cpu_images)
     print(json.dumps(line), flush=True)

@@ -188,6 +188,15 @@ FUSION_API int fusion_debug_state(fusion_model* m, const float* images,
                                   int32_t* live_out, int* n_live,
                                   void* stream);
 
+/* Diagnostic (race proxy): fill the model's floating-point workspace (the
+ * fp32 residual stream and token sizes, the activation, q|k|v, MLP, head and
+ * CLS-score buffers) with NaN bytes, asynchronously on the stream.  A run
+ * enqueued afterwards must give bit-identical outputs to an unpoisoned run:
+ * every value a run reads is written earlier in the same run.  The integer
+ * maps (row map, offsets, live map, counts, keep flags) are not touched.
+ * Errors: FUSION_E_INVALID_ARG, FUSION_E_HIP. */
+FUSION_API int fusion_debug_poison_workspace(fusion_model* m, void* stream);
+
 /* Per-kernel timing for measurement: when enabled, runs record a pair of
  * HIP events around every launch on the run's stream and accumulate the
  * elapsed time per kernel kind once fusion_profile_read synchronises.

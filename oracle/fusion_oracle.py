@@ -57,8 +57,8 @@ Readings of the paper where it is silent (each also listed in the design doc):
 
 Decision margins (in O(1) units) are logged for every discrete decision:
 argmax best - second similarity, top-r gap s_(r) - s_(r+1), router: the
-change of m that moves the count expression across an integer (unclamped
-only), exit |c - delta|, prune N (s_(k) - s_(k+1)) for CLS-attention scores
+distance of the count expression to the nearest integer (unclamped only),
+exit |c - delta|, prune N (s_(k) - s_(k+1)) for CLS-attention scores
 (probabilities of order 1/N) and s_(k) - s_(k+1) for learned scores.
 
 Follow mode: given another implementation's decisions (``follow``), the
@@ -282,10 +282,10 @@ def router(x_cls, w, beta, rho, r_b, N, rule="budget"):
     "budget":   r = clamp(floor(2 rho m r_b + 1/2), 0, floor(N/2));
     "fraction": r = min(floor(((rho m) N) / 2), floor(N/2)) (Sec. III-C
                 with the rescaled ratio of Eq. 5).
-    Returns (m, r, margin).  The margin is in units of m, like every other
-    decision margin in O(1) units: the distance of the count expression to
-    the nearest integer divided by its slope in m, i.e. how far m must move
-    to change r; +inf when the count is clamped or does not depend on m.
+    Returns (m, r, margin).  The margin is the distance of the count
+    expression (2 rho m r_b + 1/2, or rho m N / 2) to the nearest integer,
+    in units of the count, i.e. how far the expression must move to change
+    r; +inf when the count is clamped or does not depend on m.
     """
     z = F32(np.dot(w, x_cls)) + F32(beta)
     m = F32(1.0) / (F32(1.0) + np.exp(-z, dtype=F32))
@@ -297,7 +297,7 @@ def router(x_cls, w, beta, rho, r_b, N, rule="budget"):
         slope = 2.0 * float(rho) * float(r_b)
     r_raw = math.floor(t)
     r = min(max(r_raw, 0), N // 2)
-    margin = abs(t - round(t)) / slope if (r == r_raw and slope > 0) else math.inf
+    margin = abs(t - round(t)) if (r == r_raw and slope > 0) else math.inf
     return m, int(r), margin
 
 
@@ -419,16 +419,18 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
             dst_origin}, "exit": bool, "ids": [origin ids after the block's
             adaptation]}} from another implementation (see module doc).
     tol:    decision margin under which a followed choice may differ; a
-            float, or {"exit": t_exit, "other": t[, "prune": t_prune]} to
-            give the exit rule (units of c) and the prune rule (score
-            units) their own margins.
+            float, or {"exit": t_exit, "other": t[, "prune": t_prune]
+            [, "router": t_router]} to give the exit rule (units of c), the
+            prune rule (score units) and the merge count (count units) their
+            own margins.
     Returns dict(logits, exit_block, token_counts[L], trace, adopted).
     """
     L = cfg["L"]
     if isinstance(tol, dict):
-        tol_exit, tol_prune, tol = tol["exit"], tol.get("prune", tol["other"]), tol["other"]
+        tol_exit, tol_prune = tol["exit"], tol.get("prune", tol["other"])
+        tol_router, tol = tol.get("router", tol["other"]), tol["other"]
     else:
-        tol_exit = tol_prune = tol
+        tol_exit = tol_prune = tol_router = tol
     if delta is None:
         delta = cfg["delta"]
     delta_of = {b: F32(dl) for b, dl in zip(cfg["exits"], delta)}
@@ -457,7 +459,7 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
                                    rho, cfg["r_b"][b - 1], N, merge_rule)
             tb.update(m=float(m), r=r, router_margin=rmargin)
             if fb is not None and fb["r"] != r:
-                if not (rmargin < tol and abs(fb["r"] - r) == 1):
+                if not (rmargin < tol_router and abs(fb["r"] - r) == 1):
                     raise DecisionMismatch(
                         f"block {b}: r {fb['r']} vs oracle {r} (margin {rmargin})")
                 adopted.append((b, "r"))

@@ -79,6 +79,7 @@ SIGNATURES = [
     ("fusion_debug_state", c_int, [c_void_p, c_void_p, c_int, c_int, c_int,
                                    c_void_p, c_void_p, c_void_p,
                                    POINTER(c_int), c_void_p]),
+    ("fusion_debug_poison_workspace", c_int, [c_void_p, c_void_p]),
     ("fusion_profile_enable", c_int, [c_void_p, c_int]),
     ("fusion_profile_kinds", c_int, []),
     ("fusion_profile_kind_name", c_char_p, [c_int]),

@@ -787,6 +787,31 @@ FUSION_API int fusion_debug_state(fusion_model* m, const float* images, int batc
   return rc;
 }
 
+FUSION_API int fusion_debug_poison_workspace(fusion_model* m, void* stream) {
+  if (int rc = check_model(m)) return rc;
+  HIP_OR_FAIL(hipSetDevice(m->device));
+  hipStream_t s = (hipStream_t)stream;
+  const Config& c = m->cfg;
+  const size_t esz = c.precision == 1 ? 2 : 4;
+  const size_t Mmax = (size_t)m->max_batch * (c.n0 + 1);
+  const size_t ffn_cols = std::max<size_t>(c.mlp, c.pdim);
+  // all-ones bytes: NaN in fp32 and in bf16
+  struct Buf { void* p; size_t bytes; };
+  const Buf bufs[] = {
+      {m->x, Mmax * c.d * 4},
+      {m->size[0], Mmax * 4}, {m->size[1], Mmax * 4},
+      {m->act, Mmax * c.d * esz},
+      {m->qkv, Mmax * 3 * c.d * esz},
+      {m->ffn, Mmax * ffn_cols * esz},
+      {m->hc, (size_t)m->max_batch * c.d * esz},
+      {m->hbuf, (size_t)m->max_batch * std::max(c.exit_hidden, 1) * esz},
+      {m->head_buf, (size_t)m->max_batch * c.C * 4},
+      {m->cls_scores, (size_t)m->max_batch * c.heads * (c.n0 + 1) * 4},
+  };
+  for (const Buf& b : bufs) HIP_OR_FAIL(hipMemsetAsync(b.p, 0xFF, b.bytes, s));
+  return FUSION_OK;
+}
+
 FUSION_API int fusion_profile_enable(fusion_model* m, int on) {
   if (!m) return fail(FUSION_E_INVALID_ARG, "model is null");
   for (auto& r : m->recs) {

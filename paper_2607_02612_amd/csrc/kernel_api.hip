@@ -147,7 +147,7 @@ int compact(const fusion_ragged* in, const StepScratch& sc, int T_ub,
 }
 
 int merge_impl(const fusion_ragged* in, const int32_t* r, int id_stride, int32_t* merge_dst,
-               const fusion_packed_out* out, hipStream_t s, char* scratch, size_t scratch_cap,
+               const fusion_packed_out* out, hipStream_t s, char* mem, size_t mem_cap,
                int* M_out) {
   int M = 0, T_ub = 0;
   if (int rc = check_ragged(in, &M, &T_ub)) return rc;
@@ -160,9 +160,9 @@ int merge_impl(const fusion_ragged* in, const int32_t* r, int id_stride, int32_t
   }
   if (merge_dst && (id_stride < 1 || id_stride > (1 << 20))) return bad("id_stride out of range");
   *M_out = M;
-  if (!scratch) return FUSION_OK;  // sizing pass
-  if (step_scratch_bytes(in->batch, M) > scratch_cap) return bad("scratch too small");
-  StepScratch sc = carve(scratch, in->batch, M);
+  if (!mem) return FUSION_OK;  // sizing pass
+  if (step_scratch_bytes(in->batch, M) > mem_cap) return bad("scratch too small");
+  StepScratch sc = carve(mem, in->batch, M);
   if (int rc = prepare(in, r, M, sc, s)) return rc;
   AdaptArgs a{};
   a.x = in->x; a.rmap = sc.rmap; a.size = sc.size; a.origin = in->origin;

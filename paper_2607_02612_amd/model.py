@@ -150,6 +150,10 @@ class FusionModel:
         live_h = live[:nl].cpu().numpy()
         return [x_h[cu_h[j]:cu_h[j + 1]] for j in range(nl)], live_h
 
+    def poison_workspace(self, stream=None):
+        """Fill the floating-point workspace with NaN (race proxy)."""
+        check(self._lib.fusion_debug_poison_workspace(self._h, _stream_ptr(stream)))
+
     # ---- measurement
     def profile_enable(self, on: bool):
         check(self._lib.fusion_profile_enable(self._h, 1 if on else 0))

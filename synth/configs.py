@@ -101,6 +101,50 @@ PROFILES = {
 }
 
 
+# Tab. VII rows (Sec. IV-F, Ablation Study) as layer-set overrides of a
+# Tab. I workload, each with the profile it runs under.  "parallel prune +
+# exit" prunes at blocks that every sample reaches before the first exit
+# head; "full sequential, fixed r" merges a fixed budget with zero routers
+# (the budget rule at m = 1/2 merges exactly r pairs).  ABLATION is the
+# DeiT-S (deit_s_paper) version, ABLATION_TINY the same compositions on the
+# four-block tiny_paper shape.
+ABLATION = [
+    ("plain", dict(merges=(), exits=(), prunes=()), "balanced"),
+    ("pruning only", dict(merges=(), exits=()), "balanced"),
+    ("merging only", dict(exits=(), prunes=()), "balanced"),
+    ("early exit only", dict(merges=(), prunes=()), "balanced"),
+    ("parallel prune + exit", dict(merges=(), prunes=(3, 6, 9)), "balanced"),
+    ("sequential exit -> prune", dict(merges=()), "balanced"),
+    ("full sequential, fixed r=8 merges", dict(merge_rule="budget", r=8), "balanced"),
+    ("full sequential, merge routers", dict(), "balanced"),
+    ("full sequential, routers + power_save scaling", dict(), "power_save"),
+]
+ABLATION_SUPERSET_PRUNES = (3, 6, 9, 10)
+
+ABLATION_TINY = [
+    ("plain", dict(merges=(), exits=(), prunes=()), "balanced"),
+    ("pruning only", dict(merges=(), exits=()), "balanced"),
+    ("merging only", dict(exits=(), prunes=()), "balanced"),
+    ("early exit only", dict(merges=(), prunes=()), "balanced"),
+    ("parallel prune + exit", dict(merges=(), prunes=(1, 2)), "balanced"),
+    ("sequential exit -> prune", dict(merges=()), "balanced"),
+    ("full sequential, fixed r=4 merges", dict(merge_rule="budget", r=4), "balanced"),
+    ("full sequential, merge routers", dict(), "balanced"),
+    ("full sequential, routers + power_save scaling", dict(), "power_save"),
+]
+ABLATION_TINY_SUPERSET_PRUNES = (1, 2, 3, 4)
+
+
+def ablation_config(base: str, over: dict, **extra) -> dict:
+    """The workload of one ablation row (no exit heads: no kinds or
+    thresholds either)."""
+    o = dict(over)
+    if "exits" in o and not o["exits"]:
+        o.update(exit_kind=(), delta=())
+    o.update(extra)
+    return get(base, **o)
+
+
 def profile_settings(name: str, ref: str = "balanced") -> dict:
     """delta and rho of a named profile (Eq. 5 ratio against ``ref``)."""
     p, r = PROFILES[name], PROFILES[ref]

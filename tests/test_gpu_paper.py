@@ -61,19 +61,28 @@ def test_deit_s_paper_fp32_small_batch(torch_cuda):
         _report(f"deit_s_paper fp32 delta={delta}", worst, adopted, 8, res, cfg)
 
 
-@pytest.mark.parametrize("delta", [(0.8, 0.95), (1.0, 1.0)])
-def test_deit_s_paper_full_batch_sampled(torch_cuda, delta):
+@pytest.mark.parametrize("profile", ["balanced", "power_save", "inert exits"])
+def test_deit_s_paper_all_samples(torch_cuda, profile):
+    """Tab. I workload, all 256 samples, under the balanced profile
+    (delta = (0.8, 0.95), rho = 1), the power_save profile (delta = (0.7,
+    0.9), rho = 5/3: Eq. 5 with tau_tgt 0.5 against 0.7) and with the exit
+    heads disabled (every sample reaches both prune blocks)."""
+    from synth import configs
     torch = torch_cuda
     cfg, W, imgs = pu.make("deit_s_paper")
-    print(f"[deit_s_paper b256] delta={delta}", flush=True)
+    if profile == "inert exits":
+        delta, rho = (1.0, 1.0), 1.0
+    else:
+        st = configs.profile_settings(profile)
+        delta, rho = st["delta"], st["rho"]
+    print(f"[deit_s_paper b256] {profile}: delta={delta} rho={rho:.4f}", flush=True)
     m = pu.gpu_model(cfg, W, cfg["batch"])
-    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=list(delta))
-    # samples that reach the prune blocks are the ones to check first
-    late = [i for i in range(cfg["batch"]) if res["exit_block"][i] > 8]
-    idx = sorted(set([0, 128, 255] + late[:3]))
-    worst, adopted = pu.check_samples(cfg, W, imgs, res, idx, delta=list(delta))
-    _report("deit_s_paper", worst, adopted, len(idx), res, cfg)
-    if delta == (1.0, 1.0):
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=list(delta), rho=rho)
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]),
+                                      delta=list(delta), rho=rho)
+    _report(f"deit_s_paper {profile}", worst, adopted, cfg["batch"], res, cfg)
+    pu.adoption_report(f"deit_s_paper {profile}", adopted, cfg["batch"])
+    if profile == "inert exits":
         assert (res["exit_block"] == cfg["L"]).all()
         # tokens: 197 -> three merges -> two prunes at keep 0.7
         assert (res["counts"][:, 11] < res["counts"][:, 8]).all()

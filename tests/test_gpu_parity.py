@@ -1,13 +1,16 @@
 """End-to-end GPU parity of the staged pipeline (merge -> exit -> prune) with
 the CPU oracle, through the C ABI (fusion_run_traced).
 
-Every compared sample must take the oracle's decisions (merge pairs, r,
-exit block, kept token ids, token counts) except at decisions whose oracle
-margin is below 1e-3, where the oracle adopts the GPU's choice after
-checking it is one of the near-tied options; logits must agree within 1e-4
-(fp32 workload) or 2e-2 (bf16 workloads).  Full-size workloads are run at
-their whole batch on the GPU and sampled for the oracle (each sample is
-independent of the rest of the batch).
+Every sample must take the oracle's decisions (merge pairs, r, exit block,
+kept token ids, token counts) except at decisions whose oracle margin is
+below the decision tolerance (1e-3; on the bf16 path the exit and router
+margins are raised to 2.5x the oracle's own drift where that is larger),
+where the oracle adopts the GPU's choice after checking it is one of the
+near-tied options; adoptions are reported by kind and bounded.  Logits
+agree within 1e-4 (fp32 workload), the literal 2e-2 where the heads have
+the workload's N(0, 0.02) weights, and otherwise within 2.5x the oracle's
+own summation-order drift under the gain-amplified heads.  Every sample of
+every full-size batch is compared.
 """
 import numpy as np
 import pytest
@@ -28,6 +31,7 @@ def torch_cuda():
 def _report(tag, worst, adopted, n):
     print(f"[{tag}] samples={n} max|dlogit|={worst:.3e} near-tie adoptions={len(adopted)}",
           flush=True)
+    pu.adoption_report(tag, adopted, n)
 
 
 @pytest.mark.parametrize("affine,router_std", [("plain", 0.02), ("random", 0.2)])
@@ -57,7 +61,9 @@ def test_deit_ti_bf16_all_samples(torch_cuda, affine, router_std, rho):
 
 
 @pytest.mark.parametrize("e", [0.0, 0.5, 0.9])
-def test_deit_s_full_batch_sampled(torch_cuda, e):
+def test_deit_s_all_samples(torch_cuda, e):
+    """Headline workload, every one of the 256 samples, at the 0 / 50 / 90 %
+    early-exit thresholds."""
     torch = torch_cuda
     cfg, W, imgs = pu.make("deit_s")
     delta = pu.exit_thresholds("deit_s", 1.0)[e]
@@ -73,34 +79,67 @@ def test_deit_s_full_batch_sampled(torch_cuda, e):
     lo, hi = int((c_hat >= delta + et).sum()), int((c_hat >= delta - et).sum())
     if e == 0.0:
         lo = hi = 0
-    print(f"  early exits {n_early} (oracle window {lo}..{hi})")
+    print(f"  early exits {n_early} (oracle: {int(round(e * cfg['batch']))}, window {lo}..{hi})")
     assert lo <= n_early <= hi
-    idx = [0, 1, 77, 128, 200, 255]
-    worst, adopted = pu.check_samples(cfg, W, imgs, res, idx, delta=[delta, delta])
-    _report("deit_s", worst, adopted, len(idx))
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]),
+                                      delta=[delta, delta])
+    _report("deit_s", worst, adopted, cfg["batch"])
 
 
-def test_deit_b_full_batch_sampled(torch_cuda):
+def test_deit_s_literal_heads_all_samples_literal_bound(torch_cuda):
+    """The headline shape (DeiT-S, batch 256, bf16, merge r = 8 at every
+    block, prune keep 0.7 at blocks 4 / 7 / 10) with every weight N(0, 0.02)
+    as the workload states, exit heads included, and exits disabled: all 256
+    samples take the oracle's decisions and their logits agree within the
+    literal 2e-2."""
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_s", exit_gain=0.02 * np.sqrt(384))
+    print("[deit_s b256 literal init] delta=1 rho=1", flush=True)
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[1.0, 1.0])
+    assert np.all(res["exit_block"] == cfg["L"])
+    assert res["counts"][:, -1].max() < cfg["N0"] + 1    # merged and pruned
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]),
+                                      delta=[1.0, 1.0], logit_bound=2e-2)
+    _report("deit_s literal", worst, adopted, cfg["batch"])
+    assert worst <= 2e-2
+
+
+def test_untraced_run_equals_traced_run(torch_cuda):
+    """fusion_run (the timed path) and fusion_run_traced give bit-identical
+    logits, exit blocks and token counts at the headline workload."""
+    torch = torch_cuda
+    cfg, W, imgs = pu.make("deit_s")
+    delta = pu.exit_thresholds("deit_s", 1.0)[0.5]
+    m = pu.gpu_model(cfg, W, cfg["batch"])
+    x = torch.from_numpy(imgs).cuda()
+    a = pu.gpu_run(m, x, delta=[delta, delta], traced=True)
+    b = pu.gpu_run(m, x, delta=[delta, delta], traced=False)
+    for k in ("logits", "exit_block", "counts"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_deit_b_all_samples(torch_cuda):
     torch = torch_cuda
     cfg, W, imgs = pu.make("deit_b")
     print("[deit_b b256]", flush=True)
     m = pu.gpu_model(cfg, W, cfg["batch"])
     res = pu.gpu_run(m, torch.from_numpy(imgs).cuda())
-    worst, adopted = pu.check_samples(cfg, W, imgs, res, [0, 131, 255])
-    _report("deit_b", worst, adopted, 3)
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]))
+    _report("deit_b", worst, adopted, cfg["batch"])
 
 
 @pytest.mark.parametrize("rho", [0.5, 1.0, 1.5])
-def test_deit_s_384_sampled(torch_cuda, rho):
+def test_deit_s_384_all_samples(torch_cuda, rho):
     torch = torch_cuda
     cfg, W, imgs = pu.make("deit_s_384")
     delta = pu.exit_thresholds("deit_s_384", rho)[0.5]
     print(f"[deit_s_384 b64] rho={rho} delta={delta}", flush=True)
     m = pu.gpu_model(cfg, W, cfg["batch"])
     res = pu.gpu_run(m, torch.from_numpy(imgs).cuda(), delta=[delta, delta], rho=rho)
-    worst, adopted = pu.check_samples(cfg, W, imgs, res, [0, 33, 63],
+    worst, adopted = pu.check_samples(cfg, W, imgs, res, range(cfg["batch"]),
                                       delta=[delta, delta], rho=rho)
-    _report("deit_s_384", worst, adopted, 3)
+    _report("deit_s_384", worst, adopted, cfg["batch"])
 
 
 @pytest.mark.parametrize("name", ["deit_ti", "deit_s"])

@@ -62,15 +62,15 @@ def test_fraction_rule_closed_form(p, N, rho, want):
     assert margin >= 0.0
 
 
-def test_fraction_rule_margin_is_distance_in_m():
-    # m = 0.2501 at N = 196: t = 24.5098, nearest integer 24.5 -> no; the
-    # count changes when t crosses 25 (m = 25/98) or 24 (m = 24/98)
+def test_fraction_rule_margin_is_distance_in_count_units():
+    # m = 0.2501 at N = 196: t = m * 98 = 24.51; the count changes when t
+    # crosses 25 or 24, so the margin is the distance to the nearer one
     beta = math.log(0.2501 / 0.7499)
     m, r, margin = fo.router(np.zeros(4, np.float32), np.zeros(4, np.float32),
                              beta, 1.0, 0, 196, "fraction")
     assert r == 24
     t = float(m) * 98.0
-    assert margin == pytest.approx(min(t - 24.0, 25.0 - t) / 98.0, rel=1e-9)
+    assert margin == pytest.approx(min(t - 24.0, 25.0 - t), rel=1e-9)
 
 
 def test_fraction_rule_ignores_budget_and_budget_rule_is_unchanged():

@@ -56,7 +56,7 @@ def test_router_sigmoid_and_margin():
     z = 0.5 * 2 - 0.25 * 4 + 0.3
     assert abs(float(m) - 1 / (1 + math.exp(-z))) < 1e-7
     t = 2 * float(m) * 8 + 0.5
-    assert r == math.floor(t) and abs(margin - abs(t - round(t)) / 16) < 1e-12
+    assert r == math.floor(t) and abs(margin - abs(t - round(t))) < 1e-12
 
 
 @pytest.mark.parametrize("N", [0, 1, 5, 137, 196, 576])
