@@ -304,6 +304,24 @@ FUSION_API int fusion_test_merge(const fusion_ragged* in, const int32_t* r, int 
                                  int32_t* merge_dst, const fusion_packed_out* out,
                                  void* stream);
 
+/* fusion_test_merge without any device allocation, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, checks and results as
+ * fusion_test_merge.  Its scratch is a static device array of the library
+ * (FUSION_NOALLOC_SCRATCH_BYTES, one per GPU, held until the process ends);
+ * a call needs 12 bytes per row plus 16 per sample (each part rounded up to
+ * 256 bytes), so batch 256 at 197 tokens takes about 0.6 MiB.  The call
+ * makes no allocation and does not synchronise: it is asynchronous on the
+ * stream like fusion_run (the host offsets and counts are copied in before
+ * it returns).  Every call on one GPU shares that GPU's array: calls that
+ * overlap (other streams, other threads) race, so serialise them.  Errors:
+ * FUSION_E_CAPACITY when the call needs more scratch than the array holds,
+ * otherwise as fusion_test_merge. */
+#define FUSION_NOALLOC_SCRATCH_BYTES (1u << 20)
+FUSION_API int fusion_test_merge_noalloc(const fusion_ragged* in, const int32_t* r,
+                                         int id_stride, int32_t* merge_dst,
+                                         const fusion_packed_out* out, void* stream);
+
 /* Exit check (Eq. 7; optional), top-k pruning of the samples that continue
  * (Eq. 8) and re-compaction.  Token scores: the head mean of CLS-attention
  * probabilities, scores = device fp32 [batch][heads][tmax] laid out as

@@ -93,6 +93,8 @@ SIGNATURES = [
                                       c_void_p]),
     ("fusion_test_merge", c_int, [POINTER(FusionRagged), c_void_p, c_int, c_void_p,
                                   POINTER(FusionPackedOut), c_void_p]),
+    ("fusion_test_merge_noalloc", c_int, [POINTER(FusionRagged), c_void_p, c_int, c_void_p,
+                                          POINTER(FusionPackedOut), c_void_p]),
     ("fusion_test_topk_compact", c_int, [POINTER(FusionRagged), c_void_p, c_int, c_int,
                                          c_void_p, c_void_p, c_double, c_void_p, c_int,
                                          c_float, c_void_p, c_void_p, c_int, c_void_p,

@@ -9,12 +9,21 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 
 #include "../../include/fusion.h"
 #include "kernels.h"
 
 using namespace fusion;
+
+// Scratch of fusion_test_merge_noalloc: a static device array, one copy per
+// GPU the library runs on, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is a stand-in, not a
+// device address): its address on the current device comes from
+// hipGetSymbolAddress, looked up once per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)1 << 20;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -178,6 +187,27 @@ int merge_impl(const fusion_ragged* in, const int32_t* r, int id_stride, int32_t
   return compact<float>(in, sc, T_ub, nullptr, nullptr, nullptr, out, s);
 }
 
+// Device address of `scratch` on the current device, looked up on the
+// first call on each device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+int noalloc_scratch(char** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return bad("device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    HIP_TRY(hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return api_fail(FUSION_E_HIP, "no device address for the static scratch");
+    g_scratch_ptr[dev] = (char*)ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return FUSION_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -250,6 +280,26 @@ FUSION_API int fusion_test_merge(const fusion_ragged* in, const int32_t* r, int 
   const size_t need = step_scratch_bytes(in->batch, M);
   HIP_TRY(mem.alloc(need));
   return merge_impl(in, r, id_stride, merge_dst, out, s, mem.p, need, &M);
+}
+
+FUSION_API int fusion_test_merge_noalloc(const fusion_ragged* in, const int32_t* r,
+                                         int id_stride, int32_t* merge_dst,
+                                         const fusion_packed_out* out, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  int M = 0;
+  if (int rc = merge_impl(in, r, id_stride, merge_dst, out, s, nullptr, 0, &M)) return rc;
+  const size_t need = step_scratch_bytes(in->batch, M);
+  if (need > kNoAllocScratchBytes)
+    return api_fail(FUSION_E_CAPACITY,
+                    ("the call needs " + std::to_string(need) + " bytes of scratch; the static " +
+                     "array holds " + std::to_string(kNoAllocScratchBytes))
+                        .c_str());
+  char* mem = nullptr;
+  if (int rc = noalloc_scratch(&mem)) return rc;
+  // every scratch word the kernels read is written earlier in this call
+  // (offsets, counts and sizes copied in, maps set by the init kernel, keep
+  // flags and new lengths by the adapt kernel), so nothing is cleared
+  return merge_impl(in, r, id_stride, merge_dst, out, s, mem, kNoAllocScratchBytes, &M);
 }
 
 FUSION_API int fusion_test_topk_compact(const fusion_ragged* in, const float* scores, int heads,

@@ -106,9 +106,10 @@ def _packed(M, B, dev):
     return o, po
 
 
-def merge(x, size, origin, cu, r, id_stride):
+def merge(x, size, origin, cu, r, id_stride, noalloc=False):
     """Bipartite merge of r[i] pairs per sample (x updated in place); returns
-    (packed output dict, merge_dst [B, id_stride] int32)."""
+    (packed output dict, merge_dst [B, id_stride] int32).  noalloc: the
+    variant whose scratch is the library's static device array."""
     rg, cu_h = _ragged(x, size, origin, cu)
     B = len(cu_h) - 1
     r_h, r_p = _host_i32(r)
@@ -116,8 +117,8 @@ def merge(x, size, origin, cu, r, id_stride):
         raise ValueError("one merge count per sample")
     o, po = _packed(x.shape[0], B, x.device)
     md = torch.full((B, id_stride), -1, dtype=torch.int32, device=x.device)
-    check(_native.lib().fusion_test_merge(byref(rg), r_p, id_stride, md.data_ptr(), byref(po),
-                                          _stream()))
+    fn = _native.lib().fusion_test_merge_noalloc if noalloc else _native.lib().fusion_test_merge
+    check(fn(byref(rg), r_p, id_stride, md.data_ptr(), byref(po), _stream()))
     return o, md
 
 

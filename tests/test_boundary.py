@@ -193,3 +193,15 @@ def test_kernel_level_entry_points_reject_bad_arguments_on_host():
                                         None, None, 1, None, None, None, br(po), None) == -1
     assert lib.fusion_test_topk_compact(br(rg), 8, 1, 4, None, None, 0.5, None, 0, 1.0,
                                         None, None, 1, None, None, None, br(po), None) == -1
+
+
+def test_noalloc_merge_refuses_oversized_calls_on_host():
+    """fusion_test_merge_noalloc returns FUSION_E_CAPACITY when a call would
+    need more scratch than the static array holds, before any device call."""
+    lib = _native.lib()
+    cu, rg, po = _ragged_args(np.arange(0, 197 * 700 + 1, 197))
+    r = np.zeros(700, dtype=np.int32)
+    rc = lib.fusion_test_merge_noalloc(ctypes.byref(rg), r.ctypes.data_as(ctypes.c_void_p), 197,
+                                       None, ctypes.byref(po), None)
+    assert rc == -3, lib.fusion_last_error()
+    assert "scratch" in lib.fusion_last_error().decode()
