@@ -507,9 +507,8 @@ def run_sample(img, W, cfg, mode, delta=None, rho=1.0, follow=None,
                 score = learned_scores(x, Wb["prune_w"], Wb["prune_b"][0])
                 unit = 1.0
             kept, pmargin, order = prune_plan(score, k, unit)
-            tb.update(k=k, prune_margin=pmargin)
-            if learned:
-                tb["scores"] = score.copy()
+            tb.update(k=k, prune_margin=pmargin, scores=score.copy(),
+                      score_unit=1.0 if learned else float(N))
             if fb is not None:
                 kept = _follow_prune(b, score, k, kept, order, origin, fb["ids"],
                                      tol_prune, adopted, unit)

@@ -41,6 +41,7 @@ template <int TMAX_> struct AdSize {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+static_assert(AdSize<AD_TMAX>::AMAX == AD_SIM_STRIDE, "similarity workspace stride");
 
 __device__ __forceinline__ int merge_count(float m, double rho, int r_b, int N, int rule) {
   // budget:   r = clamp(floor(((2 rho) m) r_b + 1/2), 0, floor(N/2));
@@ -142,12 +143,15 @@ __device__ __forceinline__ int rank_lanes(int n) {
 // never wins) runs in-lane, then across the 4 lanes of a token with the
 // lane-swap instructions, then over the WC wave groups in B order through
 // LDS (pbv, pbi: WC SAG entries each).  rn holds the reciprocal norms:
-// A rows of the pass at [0, SAG), B rows at [SAG, SAG + BMAX).
+// A rows of the pass at [0, SAG), B rows at [SAG, SAG + BMAX).  Passes of SAG
+// A rows run from A row ag_first, at most n_pass of them; bestsim / best may
+// point to LDS or to global memory (indexed by A row).
 template <class Z>
 __device__ void similarity_argmax(const float* __restrict__ x, const int* prow, int d,
                                   int nA, int nB, float* rn, float* bestsim,
                                   int* best, bf16_t* Ahi, bf16_t* Alo,
-                                  bf16_t* Bhi, bf16_t* Blo, float* pbv, int* pbi) {
+                                  bf16_t* Bhi, bf16_t* Blo, float* pbv, int* pbi,
+                                  int ag_first = 0, int n_pass = 1 << 30) {
   constexpr int SKC = Z::SKC, SKP = Z::SKP, SPT = Z::SPT, NBW = Z::NBW, BG = Z::BG;
   constexpr int SAG = Z::SAG, WC = Z::WC, BMAX = Z::BMAX;
   constexpr int Q = SKC / 4;  // 16-byte slots per row and chunk
@@ -158,7 +162,7 @@ __device__ void similarity_argmax(const float* __restrict__ x, const int* prow, 
   const int g = lane >> 4, c = lane & 15;
   const int wr = wave / WC, wc = wave % WC;
   const int nbt = (nB + 15) >> 4, nck = d / SKC;
-  for (int ag = 0; ag < nA; ag += SAG) {
+  for (int ag = ag_first, pass = 0; ag < nA && pass < n_pass; ag += SAG, pass++) {
     const float* xs = x;
     uint32_t soff[SPT];  // slot offsets into x, in floats (physical row * d + feature)
     bool sval[SPT];
@@ -422,8 +426,17 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   }
   const int nA = (N + 1) / 2, nB = N / 2;
   if (r > 0) {
-    similarity_argmax<Z>(a.x, prow, d, nA, nB, rn, bestsim, best, Ahi, Alo, Bhi, Blo, pbv,
-                         pbi);
+    if (a.sim_v) {
+      // best matches computed by similarity_kernel, one workgroup per pass
+      for (int e = tid; e < nA; e += AD_NT) {
+        bestsim[e] = a.sim_v[(size_t)i * AMAX + e];
+        best[e] = a.sim_i[(size_t)i * AMAX + e];
+      }
+      __syncthreads();
+    } else {
+      similarity_argmax<Z>(a.x, prow, d, nA, nB, rn, bestsim, best, Ahi, Alo, Bhi, Blo, pbv,
+                           pbi);
+    }
     // top-r of A by best similarity, ties to the lower A slot; P adjacent
     // lanes split the comparisons of one element
     {
@@ -613,16 +626,58 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   if (tid == 0) a.newlen[i] = cnt;
 }
 
+// Best matches of the merge step for long samples, one workgroup per (live
+// sample, pass of SAG A rows): the same passes similarity_argmax makes one
+// after the other inside adapt_kernel, spread over workgroups so that a
+// small batch of long samples fills the GPU.  Results go to a.sim_v /
+// a.sim_i ([live sample][AMAX]); adapt_kernel reads them instead.
+template <class Z>
+__global__ __launch_bounds__(AD_NT) void similarity_kernel(AdaptArgs a) {
+  const int i = blockIdx.x, pass = blockIdx.y;
+  if (i >= a.cnt->nlive) return;
+  const int base = a.cu[i], T = a.cu[i + 1] - base, N = T - 1;
+  if (T > Z::TMAX || T < 1) return;
+  const int nA = (N + 1) / 2, nB = N / 2;
+  if (nB < 1 || pass * Z::SAG >= nA) return;
+  constexpr int TMAX = Z::TMAX, BMAX = Z::BMAX, SKP = Z::SKP, SAG = Z::SAG;
+  __shared__ int prow[TMAX];
+  __shared__ __attribute__((aligned(16))) float rn[TMAX];
+  __shared__ __attribute__((aligned(16))) bf16_t Ahi[2 * SAG * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Alo[2 * SAG * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bhi[2 * BMAX * SKP];
+  __shared__ __attribute__((aligned(16))) bf16_t Blo[2 * BMAX * SKP];
+  __shared__ float pbv[Z::WC * SAG];
+  __shared__ int pbi[Z::WC * SAG];
+  for (int t = threadIdx.x; t < T; t += AD_NT) prow[t] = a.rmap[base + t];
+  __syncthreads();
+  similarity_argmax<Z>(a.x, prow, a.d, nA, nB, rn, a.sim_v + (size_t)i * Z::AMAX,
+                       a.sim_i + (size_t)i * Z::AMAX, Ahi, Alo, Bhi, Blo, pbv, pbi,
+                       pass * SAG, 1);
+}
+
 hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
   if (a.nlive_ub <= 0) return hipSuccess;
+  AdaptArgs one = a;  // single-pass classes: the adapt kernel computes the matches itself
+  one.sim_v = nullptr;
+  one.sim_i = nullptr;
   if (a.T_ub <= 128 && a.d % AdSize<128>::SKC == 0) {
-    adapt_kernel<AdSize<128>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
+    adapt_kernel<AdSize<128>><<<a.nlive_ub, AD_NT, 0, s>>>(one);
   } else if (a.T_ub <= 256) {
     if (a.d % AdSize<256>::SKC != 0) return hipErrorInvalidValue;
-    adapt_kernel<AdSize<256>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
+    adapt_kernel<AdSize<256>><<<a.nlive_ub, AD_NT, 0, s>>>(one);
   } else {
-    if (a.T_ub > AD_TMAX || a.d % AdSize<AD_TMAX>::SKC != 0) return hipErrorInvalidValue;
-    adapt_kernel<AdSize<AD_TMAX>><<<a.nlive_ub, AD_NT, 0, s>>>(a);
+    typedef AdSize<AD_TMAX> Z;
+    if (a.T_ub > AD_TMAX || a.d % Z::SKC != 0) return hipErrorInvalidValue;
+    AdaptArgs b = a;
+    if (a.isM && a.sim_v && a.sim_i) {
+      // several passes of A rows: one workgroup each
+      const int passes = ((a.T_ub - 1 + 1) / 2 + Z::SAG - 1) / Z::SAG;
+      similarity_kernel<Z><<<dim3(a.nlive_ub, passes), AD_NT, 0, s>>>(a);
+    } else {
+      b.sim_v = nullptr;
+      b.sim_i = nullptr;
+    }
+    adapt_kernel<Z><<<a.nlive_ub, AD_NT, 0, s>>>(b);
   }
   return hipGetLastError();
 }

@@ -352,9 +352,17 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
 // consecutive head dimensions of one query and stores them as 8 bytes.
 constexpr int RES_NT = 512;  // 8 waves share the staged K and V^T
 
+// Long samples (17 .. 37 key tiles, T <= 592: the 384 x 384 workload) use
+// the same kernel with one workgroup per CU: K (74 KB) and V^T (78 KB) of the
+// (sample, head) fill the LDS, each wave holds a whole score row of its query
+// tile in registers (2 waves per SIMD, up to 256 VGPRs), and the staging
+// loops cover more keys than threads.
+constexpr int RES_LONG_MAXT = 37;
+
 template <int MAXT>
-__global__ __launch_bounds__(RES_NT, 4) void attention_mfma_res(AttnArgs a) {
-  static_assert(MAXT >= 1 && MAXT <= 16, "resident key range");
+__global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res(AttnArgs a) {
+  static_assert(MAXT >= 1 && MAXT <= RES_LONG_MAXT, "resident key range");
+  constexpr bool LONG = MAXT > 16;
   constexpr int TP = MAXT * 16;               // padded keys
   constexpr int NP = (MAXT + 1) / 2;          // key tile pairs
   constexpr int TPE = NP * 32;                // keys covered by tile pairs
@@ -395,14 +403,21 @@ __global__ __launch_bounds__(RES_NT, 4) void attention_mfma_res(AttnArgs a) {
     const int r = u >> 3, cc = (u & 7) * 8;
     kin[w] = *(const uint4*)(kg + (size_t)min(r, Tn - 1) * ld + cc);
   }
-  // V^T: thread = 4 keys x 8 dims block, transposed in registers
+  // V^T: thread = 4 keys x 8 dims block, transposed in registers (long
+  // samples: VR blocks per thread, RES_NT / 8 key blocks apart)
   const int kb = tid >> 3, db = (tid & 7) * 8;   // keys 4kb.., dims db..
   const bool vth = tid < 2 * TPE;
-  uint4 vin[4];
+  constexpr int VR = LONG ? (TPE / 4 + RES_NT / 8 - 1) / (RES_NT / 8) : 1;
+  uint4 vin[VR][4];
 #pragma unroll
-  for (int r = 0; r < 4; r++)
-    vin[r] = *(const uint4*)(vg + (size_t)min(kb * 4 + r, Tn - 1) * ld + db);
-  const float szr = a.size[base + min(tid, Tn - 1)];
+  for (int v = 0; v < VR; v++)
+#pragma unroll
+    for (int r = 0; r < 4; r++)
+      vin[v][r] = *(const uint4*)(vg + (size_t)min((kb + v * (RES_NT / 8)) * 4 + r, Tn - 1) * ld + db);
+  constexpr int SR = LONG ? (TP + RES_NT - 1) / RES_NT : 1;  // sizes per thread
+  float szr[SR];
+#pragma unroll
+  for (int v = 0; v < SR; v++) szr[v] = a.size[base + min(tid + v * RES_NT, Tn - 1)];
   __builtin_amdgcn_sched_barrier(0);  // every load above is in flight before any use
 #pragma unroll
   for (int w = 0; w < KU; w++) {
@@ -411,29 +426,38 @@ __global__ __launch_bounds__(RES_NT, 4) void attention_mfma_res(AttnArgs a) {
       *(uint4*)(Ks + (u >> 3) * 64 + (((u & 7) ^ ((u >> 3) & 7)) << 3)) =
           (u >> 3) < Tn ? kin[w] : make_uint4(0, 0, 0, 0);
   }
-  uint32_t in[4][4];
 #pragma unroll
-  for (int r = 0; r < 4; r++) {
-    const uint4 v = (vth && kb * 4 + r < Tn) ? vin[r] : make_uint4(0, 0, 0, 0);
-    in[r][0] = v.x; in[r][1] = v.y; in[r][2] = v.z; in[r][3] = v.w;
-  }
-  const float sz = (tid < Tn && a.prop_attn) ? szr : 1.f;
-  if (vth) {
+  for (int v = 0; v < VR; v++) {
+    const int kbv = kb + v * (RES_NT / 8);
+    const bool vthv = LONG ? kbv < TPE / 4 : vth;
+    uint32_t in[4][4];
 #pragma unroll
-    for (int j = 0; j < 8; j++) {
-      uint32_t w[2];
+    for (int r = 0; r < 4; r++) {
+      const uint4 vv = (vthv && kbv * 4 + r < Tn) ? vin[v][r] : make_uint4(0, 0, 0, 0);
+      in[r][0] = vv.x; in[r][1] = vv.y; in[r][2] = vv.z; in[r][3] = vv.w;
+    }
+    if (vthv) {
 #pragma unroll
-      for (int q = 0; q < 2; q++) {
-        const uint32_t lo = (in[2 * q][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        const uint32_t hi = (in[2 * q + 1][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        w[q] = lo | (hi << 16);
+      for (int j = 0; j < 8; j++) {
+        uint32_t w[2];
+#pragma unroll
+        for (int q = 0; q < 2; q++) {
+          const uint32_t lo = (in[2 * q][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+          const uint32_t hi = (in[2 * q + 1][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+          w[q] = lo | (hi << 16);
+        }
+        *(uint2*)(Vt + (db + j) * VTS + kbv * 4) = make_uint2(w[0], w[1]);
       }
-      *(uint2*)(Vt + (db + j) * VTS + kb * 4) = make_uint2(w[0], w[1]);
     }
   }
   // key term of the base-2 scores: log2(size) (0 without proportional
   // attention), -inf past the sample's keys
-  if (tid < TP) lnS[tid] = tid < Tn ? logf(sz) * kLog2e : -INFINITY;
+#pragma unroll
+  for (int v = 0; v < SR; v++) {
+    const int t = tid + v * RES_NT;
+    const float sz = (t < Tn && a.prop_attn) ? szr[v] : 1.f;
+    if (t < TP) lnS[t] = t < Tn ? logf(sz) * kLog2e : -INFINITY;
+  }
   __syncthreads();
 
   bf16_t* out = (bf16_t*)a.out;
@@ -570,11 +594,24 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
         FUSION_ATTN_RES(5) FUSION_ATTN_RES(6) FUSION_ATTN_RES(7) FUSION_ATTN_RES(8)
         FUSION_ATTN_RES(9) FUSION_ATTN_RES(10) FUSION_ATTN_RES(11) FUSION_ATTN_RES(12)
         FUSION_ATTN_RES(13) FUSION_ATTN_RES(14) FUSION_ATTN_RES(15) FUSION_ATTN_RES(16)
-#undef FUSION_ATTN_RES
         default: return hipErrorInvalidValue;
       }
       return hipGetLastError();
     }
+    if (a.T_ub <= 16 * RES_LONG_MAXT) {
+      const dim3 grid(a.nlive_ub, a.H);
+      switch ((a.T_ub + 15) / 16) {
+        FUSION_ATTN_RES(17) FUSION_ATTN_RES(18) FUSION_ATTN_RES(19) FUSION_ATTN_RES(20)
+        FUSION_ATTN_RES(21) FUSION_ATTN_RES(22) FUSION_ATTN_RES(23) FUSION_ATTN_RES(24)
+        FUSION_ATTN_RES(25) FUSION_ATTN_RES(26) FUSION_ATTN_RES(27) FUSION_ATTN_RES(28)
+        FUSION_ATTN_RES(29) FUSION_ATTN_RES(30) FUSION_ATTN_RES(31) FUSION_ATTN_RES(32)
+        FUSION_ATTN_RES(33) FUSION_ATTN_RES(34) FUSION_ATTN_RES(35) FUSION_ATTN_RES(36)
+        FUSION_ATTN_RES(37)
+        default: return hipErrorInvalidValue;
+      }
+      return hipGetLastError();
+    }
+#undef FUSION_ATTN_RES
     dim3 grid(a.nlive_ub, a.H, (a.T_ub + 63) / 64);
     if (a.T_ub <= 16 * 40)
       attention_mfma<40><<<grid, 256, 0, s>>>(a);

@@ -294,6 +294,8 @@ struct fusion_model {
   float* cls_scores;
   int* keep;
   int* newlen;
+  float* sim_v;  // [max_batch][AD_SIM_STRIDE] best-match similarities (long samples)
+  int* sim_i;
   // runtime parameters
   float delta[FUSION_MAX_LAYERS];  // per exit head
   double rho = 1.0;
@@ -495,6 +497,7 @@ int run_impl(fusion_model* m, const float* images, int B, float* logits,
         a.logits = logits; a.exit_block = exit_block;
         a.cls_scores = m->cls_scores; a.tmax = T0; a.tau_eff = tau_eff;
         a.keep = m->keep; a.newlen = m->newlen;
+        a.sim_v = m->sim_v; a.sim_i = m->sim_i;
         a.tr_r = tr ? tr->r : nullptr; a.tr_m = tr ? tr->m : nullptr;
         a.tr_c = tr ? tr->c : nullptr; a.tr_merge = tr ? tr->merge_dst : nullptr;
         a.nlive_ub = B; a.T_ub = T_ub;
@@ -693,6 +696,8 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
   m->cls_scores = (float*)dev_alloc<float>(m, (size_t)max_batch * c.heads * (c.n0 + 1) * 4, &rc);
   m->keep = (int*)dev_alloc<int>(m, Mmax * 4, &rc);
   m->newlen = (int*)dev_alloc<int>(m, (size_t)max_batch * 4, &rc);
+  m->sim_v = (float*)dev_alloc<float>(m, (size_t)max_batch * AD_SIM_STRIDE * 4, &rc);
+  m->sim_i = (int*)dev_alloc<int>(m, (size_t)max_batch * AD_SIM_STRIDE * 4, &rc);
   if (rc) return bail(rc);
   *out = m;
   return FUSION_OK;
@@ -807,6 +812,7 @@ FUSION_API int fusion_debug_poison_workspace(fusion_model* m, void* stream) {
       {m->hbuf, (size_t)m->max_batch * std::max(c.exit_hidden, 1) * esz},
       {m->head_buf, (size_t)m->max_batch * c.C * 4},
       {m->cls_scores, (size_t)m->max_batch * c.heads * (c.n0 + 1) * 4},
+      {m->sim_v, (size_t)m->max_batch * AD_SIM_STRIDE * 4},
   };
   for (const Buf& b : bufs) HIP_OR_FAIL(hipMemsetAsync(b.p, 0xFF, b.bytes, s));
   return FUSION_OK;

@@ -74,14 +74,19 @@ struct StepScratch {
   int* newlen;      // [B]
   int* r;           // [B]
   LiveCounts* cnt;  // nlive = B, M
+  float* sim_v;     // [B][AD_SIM_STRIDE] best matches of long samples
+  int* sim_i;
 };
 
-size_t step_scratch_bytes(int B, int M) {
+// with_sim: also the best-match buffers that let long samples spread the
+// merge similarity over several workgroups (results are identical without)
+size_t step_scratch_bytes(int B, int M, bool with_sim = false) {
   return align256((size_t)(B + 1) * 4) + 3 * align256((size_t)B * 4) +
-         3 * align256((size_t)M * 4) + align256(sizeof(LiveCounts));
+         3 * align256((size_t)M * 4) + align256(sizeof(LiveCounts)) +
+         (with_sim ? 2 * align256((size_t)B * AD_SIM_STRIDE * 4) : 0);
 }
 
-StepScratch carve(char* p, int B, int M) {
+StepScratch carve(char* p, int B, int M, bool with_sim = false) {
   StepScratch s;
   auto take = [&](size_t bytes) {
     char* q = p;
@@ -96,6 +101,8 @@ StepScratch carve(char* p, int B, int M) {
   s.size = (float*)take((size_t)M * 4);
   s.keep = (int*)take((size_t)M * 4);
   s.cnt = (LiveCounts*)take(sizeof(LiveCounts));
+  s.sim_v = with_sim ? (float*)take((size_t)B * AD_SIM_STRIDE * 4) : nullptr;
+  s.sim_i = with_sim ? (int*)take((size_t)B * AD_SIM_STRIDE * 4) : nullptr;
   return s;
 }
 
@@ -157,7 +164,7 @@ int compact(const fusion_ragged* in, const StepScratch& sc, int T_ub,
 
 int merge_impl(const fusion_ragged* in, const int32_t* r, int id_stride, int32_t* merge_dst,
                const fusion_packed_out* out, hipStream_t s, char* mem, size_t mem_cap,
-               int* M_out) {
+               int* M_out, bool with_sim) {
   int M = 0, T_ub = 0;
   if (int rc = check_ragged(in, &M, &T_ub)) return rc;
   if (int rc = check_packed_out(out)) return rc;
@@ -170,8 +177,8 @@ int merge_impl(const fusion_ragged* in, const int32_t* r, int id_stride, int32_t
   if (merge_dst && (id_stride < 1 || id_stride > (1 << 20))) return bad("id_stride out of range");
   *M_out = M;
   if (!mem) return FUSION_OK;  // sizing pass
-  if (step_scratch_bytes(in->batch, M) > mem_cap) return bad("scratch too small");
-  StepScratch sc = carve(mem, in->batch, M);
+  if (step_scratch_bytes(in->batch, M, with_sim) > mem_cap) return bad("scratch too small");
+  StepScratch sc = carve(mem, in->batch, M, with_sim);
   if (int rc = prepare(in, r, M, sc, s)) return rc;
   AdaptArgs a{};
   a.x = in->x; a.rmap = sc.rmap; a.size = sc.size; a.origin = in->origin;
@@ -182,6 +189,7 @@ int merge_impl(const fusion_ragged* in, const int32_t* r, int id_stride, int32_t
   a.r_fixed = sc.r; a.rho = 1.0; a.delta = 1.0f; a.tau_eff = 1.0;
   a.tmax = T_ub; a.keep = sc.keep; a.newlen = sc.newlen;
   a.tr_merge = merge_dst;
+  a.sim_v = sc.sim_v; a.sim_i = sc.sim_i;
   a.nlive_ub = in->batch; a.T_ub = T_ub;
   HIP_TRY(launch_adapt(a, s));
   return compact<float>(in, sc, T_ub, nullptr, nullptr, nullptr, out, s);
@@ -275,11 +283,11 @@ FUSION_API int fusion_test_merge(const fusion_ragged* in, const int32_t* r, int 
                                  void* stream) {
   hipStream_t s = (hipStream_t)stream;
   int M = 0;
-  if (int rc = merge_impl(in, r, id_stride, merge_dst, out, s, nullptr, 0, &M)) return rc;
+  if (int rc = merge_impl(in, r, id_stride, merge_dst, out, s, nullptr, 0, &M, true)) return rc;
   CallScratch mem(s);
-  const size_t need = step_scratch_bytes(in->batch, M);
+  const size_t need = step_scratch_bytes(in->batch, M, true);
   HIP_TRY(mem.alloc(need));
-  return merge_impl(in, r, id_stride, merge_dst, out, s, mem.p, need, &M);
+  return merge_impl(in, r, id_stride, merge_dst, out, s, mem.p, need, &M, true);
 }
 
 FUSION_API int fusion_test_merge_noalloc(const fusion_ragged* in, const int32_t* r,
@@ -287,7 +295,7 @@ FUSION_API int fusion_test_merge_noalloc(const fusion_ragged* in, const int32_t*
                                          const fusion_packed_out* out, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   int M = 0;
-  if (int rc = merge_impl(in, r, id_stride, merge_dst, out, s, nullptr, 0, &M)) return rc;
+  if (int rc = merge_impl(in, r, id_stride, merge_dst, out, s, nullptr, 0, &M, false)) return rc;
   const size_t need = step_scratch_bytes(in->batch, M);
   if (need > kNoAllocScratchBytes)
     return api_fail(FUSION_E_CAPACITY,
@@ -299,7 +307,7 @@ FUSION_API int fusion_test_merge_noalloc(const fusion_ragged* in, const int32_t*
   // every scratch word the kernels read is written earlier in this call
   // (offsets, counts and sizes copied in, maps set by the init kernel, keep
   // flags and new lengths by the adapt kernel), so nothing is cleared
-  return merge_impl(in, r, id_stride, merge_dst, out, s, mem, kNoAllocScratchBytes, &M);
+  return merge_impl(in, r, id_stride, merge_dst, out, s, mem, kNoAllocScratchBytes, &M, false);
 }
 
 FUSION_API int fusion_test_topk_compact(const fusion_ragged* in, const float* scores, int heads,

@@ -120,7 +120,12 @@ struct AdaptArgs {
   int* tr_merge;
   int nlive_ub;
   int T_ub;  // host bound on the tokens of every live sample (CLS included)
+  // optional workspace [nlive_ub][AD_SIM_STRIDE]: best-match similarity and
+  // index per A token, computed by a separate kernel for long samples
+  float* sim_v;
+  int* sim_i;
 };
+constexpr int AD_SIM_STRIDE = 320;  // A tokens of the longest size class (640 / 2)
 hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s);
 
 struct CompactArgs {

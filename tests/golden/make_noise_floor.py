@@ -11,11 +11,13 @@ The second run follows the first one's discrete decisions (any
 disagreement is adopted), so both share one trajectory; the only
 differences are summation order and the GELU approximation.  The maximum
 |logit difference|, |exit confidence difference|, |router count-expression
-difference| (2 rho m r_b, or rho m N / 2, in count units) and (learned
-prune scorer) |token score difference| over the sample are the floors any
+difference| (2 rho m r_b, or rho m N / 2, in count units) and |token score
+difference| before a prune (in the prune margin's units: N x probability
+for CLS-attention scores, score units for the learned scorer) over the
+sample are the floors any
 other bf16 implementation (the GPU path included) must be allowed; the
 parity tests use a multiple of them where it exceeds the literal bounds
-(2e-2 for logits, 1e-3 for exit and router margins).
+(2e-2 for logits, 1e-3 for exit, router and prune margins).
 
 Usage:  python tests/golden/make_noise_floor.py [workload ...]
         (with names: recompute only those rows of the plan, keep the rest)
@@ -99,7 +101,10 @@ def _one(args):
     with fo.accumulate("fp64"), gelu_approx():
         b_ = fo.run_sample(imgs[i], W, cfg, "bf16emu", delta=delta, rho=rho,
                            follow=f, tol=1.0)
-    ds = [float(np.abs(a["trace"][p]["scores"] - b_["trace"][p]["scores"]).max())
+    # token-score drift in the prune margin's units: score units for the
+    # learned scorer, N x probability for CLS-attention scores
+    ds = [float(a["trace"][p]["score_unit"]
+                * np.abs(a["trace"][p]["scores"] - b_["trace"][p]["scores"]).max())
           for p in cfg["prunes"] if "scores" in a["trace"].get(p, {})]
     return (float(np.abs(a["logits"] - b_["logits"]).max()),
             max(abs(a["trace"][e]["c"] - b_["trace"][e]["c"]) for e in cfg["exits"]),

@@ -67,9 +67,10 @@ def router_tol(cfg, rho=1.0):
 
 
 def prune_tol(cfg, rho=1.0):
-    """Prune-rule margin for learned scores (score units): 1e-3, raised to
-    2.5x the measured noise floor of the token scores on the bf16 path."""
-    if cfg["precision"] == "fp32" or cfg.get("prune_rule") != "learned":
+    """Prune-rule margin (score units for the learned scorer, N x probability
+    for CLS-attention scores): 1e-3, raised to 2.5x the oracle's own drift of
+    the token scores in those units on the bf16 path."""
+    if cfg["precision"] == "fp32":
         return fo.TOL
     return max(fo.TOL, FLOOR_FACTOR * noise_floor(cfg["name"], rho).get("max_dscore", 0.0))
 
@@ -170,7 +171,8 @@ def check_samples(cfg, W, imgs, res, idx, delta=None, rho=1.0, logit_bound=None)
         assert err <= tol, (i, err)
         worst = max(worst, err)
         adopted += [(int(i),) + a for a in out["adopted"]]
-        adopted.count_decisions(out["trace"])
+        adopted.count_decisions(out["trace"], {"argmax": fo.TOL, "topr": fo.TOL, "r": rtol,
+                                               "exit": etol, "prune": ptol})
         tr = res["trace"]
         for b, tb in out["trace"].items():
             if "m" in tb:
@@ -184,48 +186,62 @@ def check_samples(cfg, W, imgs, res, idx, delta=None, rho=1.0, logit_bound=None)
 
 class Adoptions(list):
     """Near-tie adoptions (sample, block, kind), with the number of
-    decisions of each kind that the oracle took on the compared samples."""
+    decisions of each kind that the oracle took on the compared samples and
+    the number of them that were eligible for adoption (oracle margin below
+    the tolerance of that kind)."""
+
+    KINDS = ("argmax", "topr", "r", "exit", "prune")
 
     def __init__(self):
         super().__init__()
-        self.decisions = {"argmax": 0, "topr": 0, "r": 0, "exit": 0, "prune": 0}
+        self.decisions = {k: 0 for k in self.KINDS}
+        self.eligible = {k: 0 for k in self.KINDS}
 
-    def count_decisions(self, trace):
+    def count_decisions(self, trace, tol):
+        inf = float("inf")
         for tb in trace.values():
             if "r" in tb:
                 self.decisions["r"] += 1
-                self.decisions["argmax"] += tb["r"]       # one best-match per merged token
-                if tb["r"] > 0 and tb.get("topr_margin", float("inf")) != float("inf"):
-                    self.decisions["topr"] += 1           # a threshold between chosen and not
+                self.eligible["r"] += tb.get("router_margin", inf) < tol["r"]
+                # one best match per merged token; all of a block's pairs
+                # count as eligible when its smallest argmax gap is
+                self.decisions["argmax"] += tb["r"]
+                self.eligible["argmax"] += tb["r"] * (tb.get("argmax_margin", inf) < tol["argmax"])
+                if tb["r"] > 0 and tb.get("topr_margin", inf) != inf:
+                    self.decisions["topr"] += 1
+                    self.eligible["topr"] += tb["topr_margin"] < tol["topr"]
             if "c" in tb:
                 self.decisions["exit"] += 1
-            if "k" in tb and tb.get("prune_margin", float("inf")) != float("inf"):
+                self.eligible["exit"] += tb.get("exit_margin", inf) < tol["exit"]
+            if "k" in tb and tb.get("prune_margin", inf) != inf:
                 self.decisions["prune"] += 1
+                self.eligible["prune"] += tb["prune_margin"] < tol["prune"]
 
 
-# Stated bounds on near-tie adoptions: every adoption is checked to lie
-# inside its decision margin, and besides that near ties must stay rare.
-# Per kind, adoptions per decision of that kind taken on the compared
-# samples (a merged token's best match, a top-r threshold, a merge count,
-# an exit check, a prune threshold), about 1.5-2x the largest rate seen over
-# the whole GPU suite: prune thresholds are near ties far more often than
-# the others because N (s_(k) - s_(k+1)) of CLS-attention probabilities,
-# about 1/N each, has gaps of order 1/N.
-ADOPTION_BOUND = {"argmax": 0.005, "topr": 0.02, "r": 0.02, "exit": 0.05, "prune": 0.20}
+# Stated bound on near-tie adoptions: each adoption is checked to lie inside
+# its decision margin; besides, at most ADOPTION_SHARE of the decisions that
+# were eligible (oracle margin below the tolerance) may go the GPU's way.  A
+# GPU whose results lie within the contract's noise lands on either side of
+# a near tie, and most eligible decisions have margins well above the actual
+# GPU-to-oracle difference, so a larger share would point at a bias rather
+# than noise.  (Eligible decisions are far more frequent for prune
+# thresholds: N (s_(k) - s_(k+1)) of CLS-attention probabilities has gaps of
+# order 1/N, below the oracle's own score drift at N of a few hundred.)
+ADOPTION_SHARE = 0.6
 
 
 def adoption_report(tag, adopted, n_samples):
-    """Print near-tie adoptions by kind (count / decisions of that kind) and
-    assert the stated bounds."""
+    """Print near-tie adoptions by kind (adopted / eligible / decisions) and
+    assert the stated bound."""
     counts = {}
     for i, b, kind in adopted:
         counts[kind] = counts.get(kind, 0) + 1
     dec = getattr(adopted, "decisions", {})
-    rates = {k: c / max(1, dec.get(k, 0)) for k, c in counts.items()}
-    print(f"[{tag}] {n_samples} samples; near-tie adoptions by kind (adopted / decisions): "
-          + ", ".join(f"{k} {counts[k]}/{dec.get(k, 0)} = {rates[k]:.4f}" for k in sorted(counts))
-          + ("" if counts else "none"), flush=True)
+    eli = getattr(adopted, "eligible", {})
+    print(f"[{tag}] {n_samples} samples; near-tie adoptions by kind "
+          f"(adopted / eligible / decisions): "
+          + (", ".join(f"{k} {counts[k]}/{eli.get(k, 0)}/{dec.get(k, 0)}" for k in sorted(counts))
+             or "none"), flush=True)
     for k, c in counts.items():
-        # (a single near tie is allowed on any sample set, however small)
-        assert c <= max(1.0, ADOPTION_BOUND[k] * dec.get(k, 0)), (tag, k, rates[k], ADOPTION_BOUND[k])
+        assert c <= ADOPTION_SHARE * eli.get(k, 0) + 1, (tag, k, c, eli.get(k, 0))
     return counts

@@ -116,7 +116,9 @@ ATT_CASES = [
     # lengths, heads, dh, precision, prop_attn
     ([1, 2, 17, 64, 197, 250, 33], 6, 64, "bf16", True),
     ([1, 2, 17, 64, 197, 250, 33], 6, 64, "bf16", False),
-    ([577, 1, 300, 129, 2, 400], 6, 64, "bf16", True),
+    ([577, 1, 300, 129, 2, 400], 6, 64, "bf16", True),   # long resident kernel (<= 592)
+    ([640, 17, 3, 599], 6, 64, "bf16", True),             # chunked kernel (593 .. 640)
+    ([260, 33, 272], 6, 64, "bf16", False),               # 17 key tiles
     ([1, 2, 33, 65, 7], 2, 32, "fp32", True),
 ]
 
