@@ -23,7 +23,7 @@ constexpr int AD_NT = 512;    // threads per workgroup (8 waves)
 // class (T <= 128, picked from the host's token bound of the block) stages
 // 64 features per chunk: its chunk loop is latency-bound, and half the
 // chunks halve the barriers.
-template <int TMAX_> struct AdSize {
+template <int TMAX_, int WC_ = (TMAX_ <= 128 ? 4 : TMAX_ <= 256 ? 2 : 4)> struct AdSize {
   static constexpr int TMAX = TMAX_;
   static constexpr int AMAX = TMAX_ / 2;
   static constexpr int BMAX = TMAX_ / 2;
@@ -31,7 +31,7 @@ template <int TMAX_> struct AdSize {
   static constexpr int SKP = SKC + 8;          // padded LDS row (bf16)
   // similarity wave layout: WC column groups of B tiles, AD_NT / 64 / WC
   // groups of 32 A rows; SAG A rows per pass
-  static constexpr int WC = TMAX_ <= 128 ? 4 : TMAX_ <= 256 ? 2 : 4;
+  static constexpr int WC = WC_;
   static constexpr int SAG = 32 * (AD_NT / 64 / WC);
   static constexpr int NBT = BMAX / 16;        // B tiles of 16 rows
   static constexpr int NBW = NBT / WC;         // B tiles per wave
@@ -667,12 +667,17 @@ hipError_t launch_adapt(const AdaptArgs& a, hipStream_t s) {
     adapt_kernel<AdSize<256>><<<a.nlive_ub, AD_NT, 0, s>>>(one);
   } else {
     typedef AdSize<AD_TMAX> Z;
+    // the split similarity: passes of 128 A rows (8 waves as 4 groups of 32
+    // A rows x 2 column groups), so that each sample's B rows are read
+    // ceil(nA / 128) times
+    typedef AdSize<AD_TMAX, 2> ZS;
+    static_assert(ZS::AMAX == Z::AMAX, "one match stride for both kernels");
     if (a.T_ub > AD_TMAX || a.d % Z::SKC != 0) return hipErrorInvalidValue;
     AdaptArgs b = a;
     if (a.isM && a.sim_v && a.sim_i) {
       // several passes of A rows: one workgroup each
-      const int passes = ((a.T_ub - 1 + 1) / 2 + Z::SAG - 1) / Z::SAG;
-      similarity_kernel<Z><<<dim3(a.nlive_ub, passes), AD_NT, 0, s>>>(a);
+      const int passes = (a.T_ub / 2 + ZS::SAG - 1) / ZS::SAG;
+      similarity_kernel<ZS><<<dim3(a.nlive_ub, passes), AD_NT, 0, s>>>(a);
     } else {
       b.sim_v = nullptr;
       b.sim_i = nullptr;
