@@ -121,16 +121,17 @@ def roofline_bound(work):
     return "mfma" if work["flop"] / BF16_PEAK >= work["byte"] / HBM_PEAK else "hbm"
 
 
-def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary
-    (profiles/traffic.json), or None if it was taken on other kernel source."""
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    counter summary (profiles/traffic.json, one entry per workload), or None
+    if none was taken there or it was taken on other kernel source."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    entry = t.get("kernels", {}).get(kernel)
+    entry = t.get("workloads", {}).get(workload, {}).get("kernels", {}).get(kernel)
     if not entry:
         return None
     src = os.path.join(ROOT, "paper_2607_02612_amd", "csrc", entry["source"])
@@ -614,13 +615,13 @@ def main():
         # with its HBM fraction on algorithmic bytes beside it
         roofline = {"kernel": dom, "bound": "mfma", "achieved": dk["tflops"],
                     "peak": BF16_PEAK / 1e12, "unit": "TFLOP/s",
-                    "frac": dk["frac_bf16_peak"], "traffic": measured_traffic(dom),
+                    "frac": dk["frac_bf16_peak"], "traffic": measured_traffic(dom, args.workload),
                     "hbm_gbps": dk["gbps"], "frac_hbm_peak": dk["frac_hbm_peak"],
                     "roof_binding_at_peaks": dk["roofline_bound"]}
     else:
         roofline = {"kernel": dom, "bound": "hbm", "achieved": dk["gbps"],
                     "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-                    "frac": dk["frac_hbm_peak"], "traffic": measured_traffic(dom)}
+                    "frac": dk["frac_hbm_peak"], "traffic": measured_traffic(dom, args.workload)}
     roofline["algorithmic_flop_per_launch"] = wk["flop"] / n_launch
     roofline["algorithmic_bytes_per_launch"] = wk["byte"] / n_launch
     roofline["mean_launch_us"] = dk["ms_per_step"] / n_launch * 1e3
