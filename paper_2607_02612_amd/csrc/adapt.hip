@@ -117,6 +117,100 @@ __device__ __forceinline__ int rank_lanes(int n) {
   return P;
 }
 
+// Order-preserving key of a float: for a, b not NaN, a < b iff
+// order_key(a) < order_key(b), and a == b iff the keys are equal (-0 and +0
+// share the key of +0).
+__device__ __forceinline__ unsigned order_key(float f) {
+  const unsigned u = f == 0.f ? 0u : __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Top-c selection over the workgroup, E (1 or 2) elements per thread:
+// e = tid (key k0, taking part if ok0) and e = tid + AD_NT (k1, ok1).  An
+// element is chosen iff it takes part and fewer than c participating
+// elements precede it, a larger key or an equal key at a lower e coming
+// first: the rank rule of the merge and prune selections (ties to the lower
+// slot), without the all-pairs comparisons.  The c-th largest key is found
+// two bits at a time from the top: per round one workgroup count of the
+// candidates whose next two bits are >= 1, >= 2 and 3 (a ballot per wave
+// and count, the wave counts in LDS slots used alternately, so one barrier
+// per round); then the elements equal to it are taken in ascending e until
+// c are chosen.  cnt: 6 * AD_NT / 64 ints of LDS; the caller synchronises
+// before reusing them.
+template <int E>
+__device__ __forceinline__ void block_top(unsigned k0, bool ok0, unsigned k1, bool ok1, int c,
+                                          bool& ch0, bool& ch1, int* cnt) {
+  constexpr int NW = AD_NT / 64;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (E < 2) ok1 = false;
+  ch0 = ch1 = false;
+  if (c <= 0) return;
+  unsigned prefix = 0, mask = 0;
+  int need = c, slot = 1;
+  for (int bit = 30; bit >= 0; bit -= 2) {
+    const bool m0 = ok0 && (k0 & mask) == prefix, m1 = ok1 && (k1 & mask) == prefix;
+    const unsigned g0 = (k0 >> bit) & 3u, g1 = (k1 >> bit) & 3u;
+    int n[3];
+#pragma unroll
+    for (int q = 0; q < 3; q++) {
+      n[q] = __popcll(__ballot(m0 && g0 >= (unsigned)(q + 1)));
+      if (E > 1) n[q] += __popcll(__ballot(m1 && g1 >= (unsigned)(q + 1)));
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int q = 0; q < 3; q++) cnt[(slot * 3 + q) * NW + wave] = n[q];
+    }
+    __syncthreads();
+    int ge[3] = {0, 0, 0};  // candidates whose next two bits are >= 1, >= 2, == 3
+#pragma unroll
+    for (int q = 0; q < 3; q++)
+#pragma unroll
+      for (int w = 0; w < NW; w++) ge[q] += cnt[(slot * 3 + q) * NW + w];
+    slot ^= 1;
+    unsigned g;
+    if (ge[2] >= need) {
+      g = 3u;
+    } else if (ge[1] >= need) {
+      g = 2u;
+      need -= ge[2];
+    } else if (ge[0] >= need) {
+      g = 1u;
+      need -= ge[1];
+    } else {
+      g = 0u;
+      need -= ge[0];
+    }
+    prefix |= g << bit;
+    mask |= 3u << bit;
+  }
+  // the elements equal to the c-th key, in ascending e: all of the first
+  // half (e < AD_NT) come before the second
+  const bool eq0 = ok0 && k0 == prefix, eq1 = ok1 && k1 == prefix;
+  const unsigned long long b0 = __ballot(eq0), b1 = E > 1 ? __ballot(eq1) : 0ull;
+  __syncthreads();
+  if (lane == 0) {
+    cnt[wave] = __popcll(b0);
+    cnt[NW + wave] = __popcll(b1);
+  }
+  __syncthreads();
+  int before0 = 0, before1 = 0, tot0 = 0;
+#pragma unroll
+  for (int w = 0; w < NW; w++) {
+    tot0 += cnt[w];
+    before0 += w < wave ? cnt[w] : 0;
+    before1 += w < wave ? cnt[NW + w] : 0;
+  }
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  const int r0 = before0 + __popcll(b0 & lt);
+  const int r1 = tot0 + before1 + __popcll(b1 & lt);
+  ch0 = ok0 && (k0 > prefix || (eq0 && r0 < need));
+  ch1 = ok1 && (k1 > prefix || (eq1 && r1 < need));
+}
+
+// Candidates above which block_top replaces the all-pairs rank count (its
+// rounds cost about as much as 256 rank comparisons per thread).
+constexpr int SEL_RADIX_MIN = 256;
+
 // Cosine similarities of the A tokens (even patch slots) with the B tokens
 // (odd slots) of one sample, and the best B for every A.
 //
@@ -358,6 +452,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   const size_t tr_row = (size_t)(a.b - 1) * a.B + orig;
 
   constexpr int TMAX = Z::TMAX, AMAX = Z::AMAX, BMAX = Z::BMAX, SKP = Z::SKP, SAG = Z::SAG;
+  static_assert(AMAX <= AD_NT && TMAX - 1 <= 2 * AD_NT, "block_top covers every candidate");
   // the host's token bound selects the size class and is exact; a sample
   // beyond it (never produced by the library itself) is dropped rather than
   // overrunning the per-token LDS arrays
@@ -389,6 +484,7 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
   __shared__ int pbi[Z::WC * SAG];
   __shared__ float red[16];
   __shared__ int ired[16];
+  __shared__ int selc[6 * AD_NT / 64];  // block_top's counts
 
   // CLS-attention scores are gathered here and follow the merge; learned
   // scores are computed after the merge from the merged hidden states
@@ -437,9 +533,15 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
       similarity_argmax<Z>(a.x, prow, d, nA, nB, rn, bestsim, best, Ahi, Alo, Bhi, Blo, pbv,
                            pbi);
     }
-    // top-r of A by best similarity, ties to the lower A slot; P adjacent
-    // lanes split the comparisons of one element
-    {
+    // top-r of A by best similarity, ties to the lower A slot: a radix
+    // selection for many candidates (nA <= AD_NT), else the rank count with
+    // P adjacent lanes splitting the comparisons of one element
+    if (nA > SEL_RADIX_MIN) {
+      const bool ok = tid < nA;
+      bool ch, unused;
+      block_top<1>(order_key(ok ? bestsim[tid] : 0.f), ok, 0u, false, r, ch, unused, selc);
+      if (ok) chosen[tid] = ch;
+    } else {
       const int P = rank_lanes(nA), p = tid % P;
       for (int e0 = 0; e0 < nA; e0 += AD_NT / P) {
         const int aa = e0 + tid / P;
@@ -592,9 +694,19 @@ __global__ __launch_bounds__(AD_NT) void adapt_kernel(AdaptArgs a) {
     for (int t = 1 + tid; t < T; t += AD_NT) ns += keepf[t];
     ns = bsum_i(ns, ired);
     const int k = (int)floor(__dmul_rn(a.tau_eff, (double)ns));
-    // rank among the kept patch tokens by score, ties to the lower slot;
-    // P adjacent lanes split the comparisons of one token
-    {
+    // top-k of the kept patch tokens by score, ties to the lower slot: a
+    // radix selection for many candidates (patch token t = 1 + e,
+    // T - 1 <= 2 AD_NT), else the rank count with P adjacent lanes
+    // splitting the comparisons of one token
+    if (T - 1 > SEL_RADIX_MIN) {
+      const int t0 = 1 + tid, t1 = 1 + AD_NT + tid;
+      const bool ok0 = t0 < T && keepf[t0], ok1 = t1 < T && keepf[t1];
+      bool ch0, ch1;
+      block_top<2>(order_key(ok0 ? sc[t0] : 0.f), ok0, order_key(ok1 ? sc[t1] : 0.f), ok1, k,
+                   ch0, ch1, selc);
+      if (t0 < T) knew[t0] = ch0;
+      if (t1 < T) knew[t1] = ch1;
+    } else {
       const int P = rank_lanes(T - 1), p = tid % P;
       for (int e0 = 0; e0 < T - 1; e0 += AD_NT / P) {
         const int t = 1 + e0 + tid / P;

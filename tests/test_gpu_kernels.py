@@ -224,6 +224,62 @@ def test_merge_ragged(torch_cuda, lengths, d):
     assert len(adopted) <= max(2, n_dec // 20)
 
 
+def _axis_tokens(rng, T, d, n_axes=3):
+    """Tokens c e_j with c = +-2^k and j among a few axes: every cosine is
+    exactly -1, 0 or 1 in any arithmetic (and the merge weights exact), so
+    the best matches and the top-r tie massively and identically on both
+    sides; ties go to the lower B slot and the lower A slot."""
+    x = np.zeros((T, d), np.float32)
+    j = rng.integers(0, n_axes, size=T)
+    c = rng.choice([-2.0, -1.0, 0.5, 1.0, 2.0, 4.0], size=T).astype(np.float32)
+    x[np.arange(T), j] = c
+    return x
+
+
+@pytest.mark.parametrize("lengths", [[97, 128, 3, 2], [197, 256, 130, 1], [577, 640, 300, 514]])
+def test_merge_exact_ties(torch_cuda, lengths):
+    """Selections among exactly equal similarities: identical to the oracle
+    with no near-tie adoption (every size class, long samples through the
+    similarity passes)."""
+    torch = torch_cuda
+    print(f"[merge ties] T={lengths}", flush=True)
+    rng = np.random.default_rng(sum(lengths))
+    d = 192
+    cu = _offsets(lengths)
+    M = int(cu[-1])
+    x = np.concatenate([_axis_tokens(rng, T, d) for T in lengths])
+    size = rng.integers(1, 4, size=M).astype(np.float32)
+    id_stride = max(lengths) + 1
+    origin = np.concatenate([np.arange(T) for T in lengths]).astype(np.int32)
+    r = np.array([min([(T - 1) // 2, (T - 1) // 3, (T - 1) // 5, 1][j % 4], (T - 1) // 2)
+                  for j, T in enumerate(lengths)], dtype=np.int32)
+    dx = torch.from_numpy(x.copy()).cuda()
+    o, md = _kern().merge(dx, torch.from_numpy(size).cuda(), torch.from_numpy(origin).cuda(),
+                          cu, r, id_stride)
+    torch.cuda.synchronize()
+    xg = dx.cpu().numpy()
+    o = {k: v.cpu().numpy() for k, v in o.items()}
+    md = md.cpu().numpy()
+    adopted = []
+    for i, T in enumerate(lengths):
+        a, b = cu[i], cu[i + 1]
+        xs, ss, og = x[a:b], size[a:b], origin[a:b].astype(np.int64)
+        plan = fo.merge_plan(xs, int(r[i]))
+        gmap = {int(s_): int(t_) for s_, t_ in enumerate(md[i]) if t_ >= 0}
+        chosen, dst = fo._follow_merge(1, plan, int(r[i]), og, gmap, 0.0, adopted)
+        if r[i] > 0:
+            assert np.array_equal(np.sort(chosen), np.sort(plan["chosen"])), i
+            assert np.array_equal(dst[np.argsort(chosen)], plan["best"][np.sort(chosen)]), i
+            xr, sr, _, orr = fo.apply_merge(xs, ss, None, og, plan["A"], plan["B"], chosen, dst)
+        else:
+            xr, sr, orr = xs, ss, og
+        p, q = o["cu"][i], o["cu"][i + 1]
+        assert np.array_equal(o["origin"][p:q], orr), i
+        assert np.array_equal(o["size"][p:q], sr), i
+        assert np.abs(xg[o["rows"][p:q]] - xr).max() <= 2e-6 * max(1.0, float(np.abs(xr).max())), i
+    assert not adopted
+
+
 # --------------------------------------------------------- prune, compact --
 def _cls_scores(rng, lengths, H, tmax):
     S = np.full((len(lengths), H, tmax), -3.0, dtype=np.float32)
@@ -288,6 +344,43 @@ def test_topk_compact_cls_attention(torch_cuda, keep, rho):
         j += 1
     assert o["counts"][0] == j
     assert o["counts"][1] == o["cu"][j]
+
+
+@pytest.mark.parametrize("lengths", [[640, 513, 514, 200, 2], [600, 97, 1, 639]])
+def test_topk_compact_exact_ties(torch_cuda, lengths):
+    """CLS-attention scores on a grid of a few values (and signed zeros,
+    which compare equal): the kept sets are decided by the lower-slot tie
+    rule on both sides and must be identical, including samples of more
+    than 513 tokens (two candidates per thread)."""
+    torch = torch_cuda
+    print(f"[topk ties] T={lengths}", flush=True)
+    rng = np.random.default_rng(len(lengths) + lengths[0])
+    H, d = 3, 64
+    cu = _offsets(lengths)
+    M, B = int(cu[-1]), len(lengths)
+    x = rng.standard_normal((M, d)).astype(np.float32)
+    size = np.ones(M, np.float32)
+    origin = np.concatenate([np.arange(T) for T in lengths]).astype(np.int32)
+    tmax = max(lengths)
+    S = np.full((B, H, tmax), -3.0, dtype=np.float32)
+    for i, T in enumerate(lengths):
+        S[i, :, :T] = rng.integers(0, 4, size=(H, T)).astype(np.float32) / 8.0
+        z = rng.random(T) < 0.3
+        S[i, :, :T][:, z] = rng.choice([0.0, -0.0], size=(H, int(z.sum()))).astype(np.float32)
+    T_ = torch.from_numpy
+    o, _, _, _ = _kern().topk_compact(T_(x).cuda(), T_(size).cuda(), T_(origin).cuda(), cu, 0.7,
+                                      scores=T_(S).cuda(), heads=H)
+    o = {k: v.cpu().numpy() for k, v in o.items()}
+    for i, T in enumerate(lengths):
+        acc = S[i, 0, :T].copy()
+        for h in range(1, H):
+            acc = acc + S[i, h, :T]
+        score = (acc / np.float32(H)).astype(np.float32)
+        k = fo.keep_count(T - 1, 0.7, 1.0)
+        kept, _, _ = fo.prune_plan(score, k)
+        rows = np.concatenate([[0], 1 + kept])
+        p, q = o["cu"][i], o["cu"][i + 1]
+        assert np.array_equal(o["rows"][p:q], cu[i] + rows), i
 
 
 def test_topk_compact_learned_scorer_fp32_ln(torch_cuda):
