@@ -28,7 +28,12 @@ template <int TMAX_, int WC_ = (TMAX_ <= 128 ? 4 : TMAX_ <= 256 ? 2 : 4)> struct
   static constexpr int AMAX = TMAX_ / 2;
   static constexpr int BMAX = TMAX_ / 2;
   static constexpr int SKC = TMAX_ <= 128 ? 64 : 32;  // features per chunk (MFMA K steps of 32)
-  static constexpr int SKP = SKC + 8;          // padded LDS row (bf16)
+  // LDS row of a staged chunk (bf16): 32-feature chunks are unpadded 64-byte
+  // rows with their four 16-byte pieces XOR-permuted by (row / 4) % 4 (the
+  // 16-byte operand reads of 16 consecutive rows then hit disjoint banks);
+  // 64-feature chunks are padded to 144-byte rows
+  static constexpr bool SWZ = SKC == 32;
+  static constexpr int SKP = SWZ ? SKC : SKC + 8;
   // similarity wave layout: WC column groups of B tiles, AD_NT / 64 / WC
   // groups of 32 A rows; SAG A rows per pass
   static constexpr int WC = WC_;
@@ -297,8 +302,10 @@ __device__ void similarity_argmax(const float* __restrict__ x, const int* prow, 
         const int r = u / Q, q = (u % Q) * 4;
         bf16_t* H = r < SAG ? Ahi + (buf * SAG + r) * SKP : Bhi + (buf * BMAX + r - SAG) * SKP;
         bf16_t* Lo = r < SAG ? Alo + (buf * SAG + r) * SKP : Blo + (buf * BMAX + r - SAG) * SKP;
-        *(uint2*)(H + q) = hv;
-        *(uint2*)(Lo + q) = lv;
+        // (SAG and BMAX are multiples of 16, so r % 16 is the LDS row's)
+        const int qs = Z::SWZ ? ((((q >> 3) ^ (r >> 2)) & 3) << 3) | (q & 4) : q;
+        *(uint2*)(H + qs) = hv;
+        *(uint2*)(Lo + qs) = lv;
       }
     };
     f32x4_t acc[2][NBW];
@@ -310,14 +317,16 @@ __device__ void similarity_argmax(const float* __restrict__ x, const int* prow, 
     const bool act = ag + 32 * wr < nA && wc * NBW < nbt;
     auto mfma = [&](int buf) {
       if (!act) return;
+      // column of this lane's 16-byte piece (rows r with r % 16 == c)
+      const int gs = Z::SWZ ? ((g ^ (c >> 2)) << 3) : 8 * g;
 #pragma unroll
       for (int kk = 0; kk < SKC / 32; kk++) {
         bf16x8_t ah[2], al[2];
 #pragma unroll
         for (int i = 0; i < 2; i++) {
           const int row = buf * SAG + 32 * wr + 16 * i + c;
-          ah[i] = *(const bf16x8_t*)(Ahi + row * SKP + 32 * kk + 8 * g);
-          al[i] = *(const bf16x8_t*)(Alo + row * SKP + 32 * kk + 8 * g);
+          ah[i] = *(const bf16x8_t*)(Ahi + row * SKP + 32 * kk + gs);
+          al[i] = *(const bf16x8_t*)(Alo + row * SKP + 32 * kk + gs);
         }
 #pragma unroll
         for (int t0 = 0; t0 < NBW; t0 += BG) {
@@ -325,8 +334,8 @@ __device__ void similarity_argmax(const float* __restrict__ x, const int* prow, 
 #pragma unroll
           for (int j = 0; j < BG; j++) {
             const int row = buf * BMAX + (wc * NBW + t0 + j) * 16 + c;
-            bh[j] = *(const bf16x8_t*)(Bhi + row * SKP + 32 * kk + 8 * g);
-            bl[j] = *(const bf16x8_t*)(Blo + row * SKP + 32 * kk + 8 * g);
+            bh[j] = *(const bf16x8_t*)(Bhi + row * SKP + 32 * kk + gs);
+            bl[j] = *(const bf16x8_t*)(Blo + row * SKP + 32 * kk + gs);
           }
 #pragma unroll
           for (int j = 0; j < BG; j++)
