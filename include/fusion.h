@@ -148,7 +148,9 @@ FUSION_API int fusion_set_exit_thresholds(fusion_model* m, const float* delta,
  * r pairs by the model's merge rule (FUSION_MERGE_*); prune blocks
  * keep floor(tau' N) patch tokens with tau' = min(1, max(0, 1 - rho (1 -
  * tau_b))).  rho = 1 is the reference profile, rho = 0 disables merging and
- * pruning.  Range [0, 16].  Errors: FUSION_E_INVALID_ARG. */
+ * pruning.  Range [0, 16].  A double, because the count expressions are
+ * evaluated in IEEE double: a float would round a ratio such as 5/3 before
+ * it enters them.  Errors: FUSION_E_INVALID_ARG. */
 FUSION_API int fusion_set_router_strength(fusion_model* m, double rho);
 
 /* Run Algorithm 1 on a batch.
