@@ -123,9 +123,12 @@ FUSION_API int fusion_blob_inspect(const void* blob, size_t blob_bytes,
  * on the bf16 path) during the call; the caller may free it afterwards.
  * max_batch: largest batch fusion_run will accept (1 .. 65536); the
  * workspace is sized for it, and max_batch * (N0 + 1) * d must stay below
- * 2^31 (the residual stream's element count).  *out receives the handle.
+ * 2^31 (the residual stream's element count) and max_batch * (N0 + 1) *
+ * max(3 d, mlp, 3 p^2) operand bytes below 2^32 (the GEMMs address their
+ * operands with 32-bit offsets; about 7,000 DeiT-S images at 224 x 224).
+ * *out receives the handle.
  * Errors: FUSION_E_INVALID_ARG, FUSION_E_BLOB (before any device call),
- * FUSION_E_CAPACITY (max_batch beyond the residual-stream limit),
+ * FUSION_E_CAPACITY (max_batch beyond either limit),
  * FUSION_E_OOM, FUSION_E_HIP. */
 FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes,
                                    int max_batch, fusion_model** out);

@@ -677,6 +677,10 @@ FUSION_API int fusion_model_create(const void* blob, size_t blob_bytes, int max_
   if (Mmax * (size_t)c.d > (size_t)INT32_MAX)
     return bail(fail(FUSION_E_CAPACITY,
                      "max_batch too large: the residual stream would exceed 2^31 elements"));
+  // the GEMM loads address their operands with 32-bit byte offsets
+  if (Mmax * std::max<size_t>(ffn_cols, 3 * (size_t)c.d) * esz > 0xFFFFFFFFull)
+    return bail(fail(FUSION_E_CAPACITY,
+                     "max_batch too large: a GEMM operand would exceed 4 GiB"));
   m->x = (float*)dev_alloc<float>(m, Mmax * c.d * 4, &rc);
   for (int k = 0; k < 2; k++) {
     m->rmap[k] = (int*)dev_alloc<int>(m, Mmax * 4, &rc);

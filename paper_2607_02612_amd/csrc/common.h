@@ -195,7 +195,10 @@ __device__ __forceinline__ float gelu_erf(float v) {
   r = r * r;
   r = r * r;
   r = r * r;
-  return fmaf(-a, r, fmaxf(v, 0.f));
+  // max(v, 0) as an integer maximum of the bit pattern (a negative float,
+  // -0 included, is a negative integer): one instruction, where the float
+  // maximum of a matrix-core result first re-canonicalises its input
+  return fmaf(-a, r, __int_as_float(max(__float_as_int(v), 0)));
 }
 
 }  // namespace fusion
