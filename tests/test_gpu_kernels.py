@@ -92,6 +92,28 @@ def test_gemm_bf16(torch_cuda, M, N, K, epi):
     assert np.array_equal(g[untouched], x0[untouched])
 
 
+@pytest.mark.parametrize("M,N,K", [(6000, 1536, 384), (20000, 1536, 384), (12000, 768, 192),
+                                   (6000, 3072, 768)])
+def test_gemm_gelu_fc1_shapes(torch_cuda, M, N, K):
+    """fc1 shapes of DeiT-Ti / S / B (K = 192, 384, 768) with hundreds to
+    thousands of 128-row tiles and a ragged last row tile: every output
+    against the float64 product + exact GELU."""
+    torch = torch_cuda
+    print(f"[gemm gelu fc1] M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + N + K)
+    A, W = _bf16(rng, (M, K)), _bf16(rng, (N, K), 0.05)
+    bias = rng.standard_normal(N).astype(np.float32) * 0.1
+    ref = A.astype(np.float64) @ W.astype(np.float64).T + bias
+    bound = np.abs(A).astype(np.float64) @ np.abs(W).astype(np.float64).T
+    out = torch.zeros(M, N, dtype=torch.bfloat16, device="cuda")
+    _kern().gemm(_to_dev_bf16(torch, A), _to_dev_bf16(torch, W), torch.from_numpy(bias).cuda(),
+                 "gelu", out)
+    g = out.float().cpu().numpy()
+    r = fo.gelu(ref.astype(np.float32))
+    err = np.abs(g - r) - (2.0 ** -8 * np.abs(r) + 1e-5 * bound + 1e-6)
+    assert (err <= 0).all(), float(err.max())
+
+
 @pytest.mark.parametrize("M,N,K,epi", [(1, 64, 64, "store"), (65, 256, 64, "gelu"),
                                        (130, 64, 256, "resid"), (9, 10, 64, "f32")])
 def test_gemm_fp32(torch_cuda, M, N, K, epi):
