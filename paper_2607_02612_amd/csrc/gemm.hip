@@ -148,6 +148,12 @@ constexpr int NXCD = 8;
 // 16-byte chunk c of staged row r (64-byte rows: four chunks)
 __device__ __forceinline__ int kslot(int r, int c) { return c ^ ((r >> 2) & 3); }
 
+// 16-byte store per lane: a wave-uniform 64-bit base in SGPRs plus the
+// lane's 32-bit byte offset
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void st16s(const void* sbase, unsigned voff, u32x4_t v) {
+  asm volatile("global_store_dwordx4 %0, %1, %2" :: "v"(voff), "v"(v), "s"(sbase) : "memory");
+}
 // global -> LDS copy of 16 bytes per lane: a wave-uniform 64-bit base in
 // SGPRs plus the lane's 32-bit byte offset (advancing to the next K step is
 // scalar arithmetic); the LDS destination is the wave-uniform m0
@@ -177,7 +183,6 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   constexpr int STGB = (MB + NB) * ROWB;              // bytes per stage
   constexpr int DMA_PER_WAVE = (MB + NB) / RPI / NWV; // DMA instructions per wave and stage
   static_assert((MB + NB) / RPI % NWV == 0, "stage split");
-  static_assert(MB * NB * 2 <= NSTG * STGB, "epilogue staging fits");
   const int M = M_dev ? *M_dev : M_host;
   const int n_nt = (N + NB - 1) / NB;
   const int id = blockIdx.x;
@@ -192,15 +197,19 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   // the accumulators start at the bias of their columns (lane l owns columns
   // n0 + wn 64 + 32 j + 8 (q / 4) + 4 (l / 32) + q % 4; columns past N, never
   // stored, take a clamped bias), so no epilogue adds it
+  // (the column base is clamped as a whole: with N % 8 == 0 the lane
+  // halves' columns c and c + 4 stay inside the bias vector; each
+  // accumulator set loads its own copy, which costs no vector ALU moves)
   f32x16_t acc[2][2];
+  const float* bias_l = e.bias + 4 * (lane >> 5);
 #pragma unroll
   for (int j = 0; j < 2; j++)
 #pragma unroll
     for (int q4 = 0; q4 < 4; q4++) {
-      const float4 bv =
-          *(const float4*)(e.bias + min(n0 + wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5), N - 4));
+      const int cb = min(n0 + wn * 64 + j * 32 + 8 * q4, N - 8);
 #pragma unroll
       for (int i = 0; i < 2; i++) {
+        const float4 bv = *(const float4*)(bias_l + cb);
         acc[i][j][4 * q4 + 0] = bv.x;
         acc[i][j][4 * q4 + 1] = bv.y;
         acc[i][j][4 * q4 + 2] = bv.z;
@@ -332,36 +341,55 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   }
 
   if (EPI == EPI_STORE || EPI == EPI_GELU) {
-    // bf16 tile -> LDS (256-byte rows, 16-byte chunk c stored at c ^ (row % 16))
-    // -> global, 16 lanes per 256-byte row segment
+    // bf16 tile -> LDS -> global, 16 lanes per 256-byte row segment.  After
+    // GELU (bound by vector instruction issue) the staged rows are 256
+    // bytes padded to 272, so that every staging address is one per-lane
+    // base plus an immediate; the plain store keeps unpadded rows with the
+    // 16-byte chunk c of row r at c ^ (r % 16) (conflict-free, and faster
+    // for the 256-row QKV tiles)
+    constexpr bool PAD = EPI == EPI_GELU;
+    constexpr int SROW = PAD ? NB * 2 + 16 : NB * 2;
+    static_assert(MB * SROW <= NSTG * STGB, "epilogue staging fits");
     __syncthreads();
+    char* sl = smem + (wm * 64 + (lane & 31)) * SROW + (PAD ? wn * 128 + (lane >> 5) * 8 : 0);
 #pragma unroll
     for (int j = 0; j < 2; j++) {
 #pragma unroll
-      for (int i = 0; i < 2; i++) {
-        const int r = wm * 64 + i * 32 + (lane & 31);
+      for (int q4 = 0; q4 < 4; q4++) {
+        // (N % 8 == 0: the lane halves' columns c and c + 4 are on the
+        // same side of N, so the check is uniform)
+        if (n0 + wn * 64 + j * 32 + 8 * q4 >= N) continue;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; q4++) {
-          const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
+        for (int i = 0; i < 2; i++) {
           float v0 = acc[i][j][4 * q4 + 0], v1 = acc[i][j][4 * q4 + 1];
           float v2 = acc[i][j][4 * q4 + 2], v3 = acc[i][j][4 * q4 + 3];
           if (EPI == EPI_GELU) {
             v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
           }
           const uint2 pk = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
-          if (n0 + c < N)
-            *(uint2*)(smem + r * (NB * 2) + (((c >> 3) ^ (r & 15)) << 4) + ((c >> 2) & 1) * 8) = pk;
+          if (PAD) {
+            *(uint2*)(sl + i * 32 * SROW + j * 64 + q4 * 16) = pk;
+          } else {
+            const int r = wm * 64 + i * 32 + (lane & 31);
+            const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
+            *(uint2*)(smem + r * SROW + (((c >> 3) ^ (r & 15)) << 4) + ((c >> 2) & 1) * 8) = pk;
+          }
         }
       }
     }
     __syncthreads();
-    bf16_t* out = (bf16_t*)e.out;
-    for (int t = tid; t < MB * (NB / 8); t += NT) {
-      const int r = t >> 4, cc = t & 15;
-      const int m = m0 + r, n = n0 + cc * 8;
-      if (m < M && n < N)
-        *(uint4*)(out + (size_t)m * e.ldo + n) =
-            *(const uint4*)(smem + r * (NB * 2) + ((cc ^ (r & 15)) << 4));
+    // lane: row tid / 16 + 16 it, 16-byte piece tid % 16; the stores take a
+    // uniform row-block base in SGPRs plus the lane's 32-bit byte offset
+    const unsigned lo = (unsigned)(((tid >> 4) * e.ldo + (tid & 15) * 8) * 2);
+    const int mr = M - m0 - (tid >> 4);   // rows from the lane's first row to M
+    const bool col_ok = n0 + (tid & 15) * 8 < N;
+#pragma unroll
+    for (int it = 0; it < MB * (NB / 8) / NT; it++) {
+      const int r = (tid >> 4) + it * (NT / 16), cc = tid & 15;
+      const u32x4_t v = PAD ? *(const u32x4_t*)(smem + r * SROW + cc * 16)
+                            : *(const u32x4_t*)(smem + r * SROW + ((cc ^ (r & 15)) << 4));
+      if (it * (NT / 16) < mr && col_ok)
+        st16s((const bf16_t*)e.out + (size_t)(m0 + it * (NT / 16)) * e.ldo + n0, lo, v);
     }
     return;
   }
