@@ -334,26 +334,31 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
 }
 
 // Resident variant for T <= 16 * MAXT <= 256 keys: one workgroup per (live
-// sample, head) stages K and V^T ([dim][key], built with an 8x8 register
-// transpose and 16-byte LDS stores) once; then each of its 8 waves walks the
-// query tiles qt = wave, wave + 8, ... with no further barrier.  Per
-// query tile the arithmetic is the chunked kernel's: transposed scores with
-// the exact row maximum, then round(E) V with the key permutation.
+// sample, head) stages K and V (both row-major, [key][dim], with 16-byte
+// LDS stores) once; then each of its 8 waves walks the query tiles qt =
+// wave, wave + 8, ... with no further barrier.  Per query tile the
+// arithmetic is the chunked kernel's: transposed scores with the exact row
+// maximum, then round(E) V with the key permutation.
 //
 // K rows are stored unpadded (128 bytes) with their eight 16-byte chunks
 // XOR-permuted by row % 8, so the per-lane 16-byte reads of 16 rows are
-// free of bank conflicts.
+// free of bank conflicts.  V rows are unpadded with their four 32-byte
+// segments XOR-permuted by (row / 2) % 2, and the V^T operand of the output
+// product is read from them with gfx950's transposing LDS read
+// (ds_read_b64_tr_b16: within each group of 16 lanes, lane i reads 4
+// consecutive 16-bit values, and lane o receives value o % 4 of lanes o / 4,
+// o / 4 + 4, o / 4 + 8 and o / 4 + 12), so no register transpose is needed.
 //
 // The key loops run over all MAXT tiles with no per-tile condition: K and
-// V^T are zero past the sample's T keys and the additive key term is -inf
+// V are zero past the sample's T keys and the additive key term is -inf
 // there (so those probabilities are exactly 0).  The host picks MAXT =
 // ceil(T_ub / 16), so at most the tiles between T and the bound are idle.
 // The output product is taken transposed (V^T . E^T), so a lane holds four
 // consecutive head dimensions of one query and stores them as 8 bytes.
-constexpr int RES_NT = 512;  // 8 waves share the staged K and V^T
+constexpr int RES_NT = 512;  // 8 waves share the staged K and V
 
 // Long samples (17 .. 37 key tiles, T <= 592: the 384 x 384 workload) use
-// the same kernel with one workgroup per CU: K (74 KB) and V^T (78 KB) of the
+// the same kernel with one workgroup per CU: K (74 KB) and V (76 KB) of the
 // (sample, head) fill the LDS, each wave holds a whole score row of its query
 // tile in registers (2 waves per SIMD, up to 256 VGPRs), and the staging
 // loops cover more keys than threads.
@@ -365,12 +370,7 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
   constexpr bool LONG = MAXT > 16;
   constexpr int TP = MAXT * 16;               // padded keys
   constexpr int NP = (MAXT + 1) / 2;          // key tile pairs
-  constexpr int TPE = NP * 32;                // keys covered by tile pairs
-  // V^T row stride (bf16): TPE + 4 makes the byte stride an odd multiple of
-  // 8, which measured fastest for the 8-byte V^T reads and the transposing
-  // stores (attention 0.294 ms per step at DeiT-S batch 256, against 0.315
-  // for TPE + 8 or + 24, 0.377 for + 16 and 0.52 for TPE itself)
-  constexpr int VTS = TPE + 4;
+  constexpr int TPE = NP * 32;                // keys covered by tile pairs (V rows)
   const int i = blockIdx.x, h = blockIdx.y;
   if (i >= a.cnt->nlive) return;
   const int base = a.cu[i], Tn = a.cu[i + 1] - base;
@@ -381,7 +381,7 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
   const float sc2 = a.scale * kLog2e;
   const bf16_t* qkv = (const bf16_t*)a.qkv;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[TP * 64];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[64 * VTS];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[TPE * 64];
   __shared__ __attribute__((aligned(16))) float lnS[TP];
   __shared__ __attribute__((aligned(16))) float clsP[TP];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -403,17 +403,14 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
     const int r = u >> 3, cc = (u & 7) * 8;
     kin[w] = *(const uint4*)(kg + (size_t)min(r, Tn - 1) * ld + cc);
   }
-  // V^T: thread = 4 keys x 8 dims block, transposed in registers (long
-  // samples: VR blocks per thread, RES_NT / 8 key blocks apart)
-  const int kb = tid >> 3, db = (tid & 7) * 8;   // keys 4kb.., dims db..
-  const bool vth = tid < 2 * TPE;
-  constexpr int VR = LONG ? (TPE / 4 + RES_NT / 8 - 1) / (RES_NT / 8) : 1;
-  uint4 vin[VR][4];
+  constexpr int VU = (TPE * 8 + RES_NT - 1) / RES_NT;  // 16-byte V pieces per thread
+  uint4 vin[VU];
 #pragma unroll
-  for (int v = 0; v < VR; v++)
-#pragma unroll
-    for (int r = 0; r < 4; r++)
-      vin[v][r] = *(const uint4*)(vg + (size_t)min((kb + v * (RES_NT / 8)) * 4 + r, Tn - 1) * ld + db);
+  for (int w = 0; w < VU; w++) {
+    const int u = tid + w * RES_NT;
+    const int r = u >> 3, cc = (u & 7) * 8;
+    vin[w] = *(const uint4*)(vg + (size_t)min(r, Tn - 1) * ld + cc);
+  }
   constexpr int SR = LONG ? (TP + RES_NT - 1) / RES_NT : 1;  // sizes per thread
   float szr[SR];
 #pragma unroll
@@ -427,28 +424,12 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
           (u >> 3) < Tn ? kin[w] : make_uint4(0, 0, 0, 0);
   }
 #pragma unroll
-  for (int v = 0; v < VR; v++) {
-    const int kbv = kb + v * (RES_NT / 8);
-    const bool vthv = LONG ? kbv < TPE / 4 : vth;
-    uint32_t in[4][4];
-#pragma unroll
-    for (int r = 0; r < 4; r++) {
-      const uint4 vv = (vthv && kbv * 4 + r < Tn) ? vin[v][r] : make_uint4(0, 0, 0, 0);
-      in[r][0] = vv.x; in[r][1] = vv.y; in[r][2] = vv.z; in[r][3] = vv.w;
-    }
-    if (vthv) {
-#pragma unroll
-      for (int j = 0; j < 8; j++) {
-        uint32_t w[2];
-#pragma unroll
-        for (int q = 0; q < 2; q++) {
-          const uint32_t lo = (in[2 * q][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-          const uint32_t hi = (in[2 * q + 1][j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-          w[q] = lo | (hi << 16);
-        }
-        *(uint2*)(Vt + (db + j) * VTS + kbv * 4) = make_uint2(w[0], w[1]);
-      }
-    }
+  for (int w = 0; w < VU; w++) {
+    const int u = tid + w * RES_NT;
+    const int r = u >> 3;
+    if (u < TPE * 8)
+      *(uint4*)(Vs + r * 64 + (((u & 7) ^ (((r >> 1) & 1) << 1)) << 3)) =
+          r < Tn ? vin[w] : make_uint4(0, 0, 0, 0);
   }
   // key term of the base-2 scores: log2(size) (0 without proportional
   // attention), -inf past the sample's keys
@@ -532,15 +513,26 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
     f32x4_t O[4];
 #pragma unroll
     for (int n = 0; n < 4; n++) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // V^T operand of key pair p, dims 16n ..: lane (g, c) needs keys
+    // 32p + 4g + 0..3 and 32p + 16 + 4g + 0..3 of dim 16n + c; with the
+    // transposing read, lane c of the group reads dims 16n + 4(c % 4) .. + 3
+    // of key Kb + c / 4 (Kb = 32p + 4g, then Kb + 16).  (Kb / 2 is even, so
+    // the key's segment permutation bit is (c / 8) % 2.)
     union VB { uint2 u[2]; bf16x8_t v; };
     VB vb[2][4];
+    const int vsb = (c >> 3) & 1;
+    const char* vlane = (const char*)Vs + (4 * g + (c >> 2)) * 128 + 8 * (c & 3);
     auto load_v = [&](int p, VB* dstv) {
 #pragma unroll
-      for (int n = 0; n < 4; n++) {
-        const bf16_t* vr = Vt + (n * 16 + c) * VTS + 32 * p + 4 * g;
-        dstv[n].u[0] = *(const uint2*)vr;
-        dstv[n].u[1] = *(const uint2*)(vr + 16);
-      }
+      for (int n = 0; n < 4; n++)
+#pragma unroll
+        for (int hh = 0; hh < 2; hh++) {
+          typedef short v4s __attribute__((ext_vector_type(4)));
+          const char* pa = vlane + (32 * p + 16 * hh) * 128 + ((n ^ vsb) << 5);
+          const v4s r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s*)pa);
+          dstv[n].u[hh] = __builtin_bit_cast(uint2, r);
+        }
     };
     load_v(0, vb[0]);
 #pragma unroll
