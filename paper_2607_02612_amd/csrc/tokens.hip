@@ -55,30 +55,37 @@ hipError_t launch_init(float* x, int* rmap, float* size, int* origin, int* cu, i
 
 // images [B, C, S, S] -> patches [B*n0, C*p*p]; patch (gy, gx) in raster
 // order, vector element (c, ky, kx).  One thread moves 4 consecutive pixels
-// of a kernel row (p % 4 == 0): a 16-byte load and one vector store, with
-// consecutive threads on consecutive pixels; 32-bit index math (the host
-// checks that B * n0 * C * p * p / 4 fits).
+// of an image row (p % 4 == 0, so they stay inside one patch): a 16-byte
+// load and one vector store.  Threads walk the images in memory order, so a
+// wave reads 1 KB of consecutive image bytes and every 128-byte line is
+// fetched by one wave (walking the patches in output order instead split
+// each line between two neighbouring patches, often handled on different
+// XCDs, and read 1.67x the image bytes from HBM); the stores are runs of
+// p / 4 lanes (32 bytes for p = 16) into one patch row.  Pixels past g p
+// (S not a multiple of p) are skipped.  32-bit index math (the host checks
+// that B * C * S * S / 4 fits).
 template <typename T>
 __global__ void patchify_kernel(const float* __restrict__ img, T* __restrict__ out,
                                 int B, int C, int S, int p) {
-  const int g = S / p, n0 = g * g, pd = C * p * p, q4 = pd / 4;
-  const int items = B * n0 * q4;
+  const int g = S / p, n0 = g * g, pd = C * p * p, sq = S / 4;
+  const int items = B * C * S * sq;
   for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < items;
        t += gridDim.x * blockDim.x) {
-    const int row = t / q4, e = (t - row * q4) * 4;
-    const int c = e / (p * p), rem = e - c * p * p;
-    const int ky = rem / p, kx = rem - ky * p;
-    const int s = row / n0, j = row - s * n0;
-    const int gy = j / g, gx = j - gy * g;
-    const float4 v = *(const float4*)(img + (((size_t)s * C + c) * S + gy * p + ky) * S + gx * p + kx);
-    Store4<T>::put(out + (size_t)row * pd + e, v);
+    const int line = t / sq, x = (t - line * sq) * 4;  // line = (s C + c) S + y
+    const int sc = line / S, y = line - sc * S;
+    const int s = sc / C, c = sc - s * C;
+    const int gy = y / p, gx = x / p;
+    if (gy >= g || gx >= g) continue;
+    const float4 v = *(const float4*)(img + (size_t)t * 4);
+    const int row = s * n0 + gy * g + gx;
+    Store4<T>::put(out + (size_t)row * pd + c * p * p + (y - gy * p) * p + (x - gx * p), v);
   }
 }
 
 template <typename T>
 hipError_t launch_patchify(const float* img, T* out, int B, int C, int S,
                            int p, hipStream_t s) {
-  const long items = (long)B * (S / p) * (S / p) * C * p * p / 4;
+  const long items = (long)B * C * S * S / 4;
   if (items >= (1L << 31) || p % 4 != 0 || S % 4 != 0) return hipErrorInvalidValue;
   int blocks = (int)((items + 255) / 256);
   if (blocks > 16384) blocks = 16384;
