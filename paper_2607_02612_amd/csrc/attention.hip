@@ -349,13 +349,16 @@ __global__ __launch_bounds__(256) void attention_mfma(AttnArgs a) {
 // consecutive 16-bit values, and lane o receives value o % 4 of lanes o / 4,
 // o / 4 + 4, o / 4 + 8 and o / 4 + 12), so no register transpose is needed.
 //
-// The key loops run over all MAXT tiles with no per-tile condition: K and
-// V are zero past the sample's T keys and the additive key term is -inf
-// there (so those probabilities are exactly 0).  The host picks MAXT =
+// The key loops run over all MAXT tiles with no per-tile condition: past
+// the sample's T keys, K and V hold finite copies of its last row and the
+// additive key term is -inf (so those probabilities are exactly 0 and the
+// copies add exact zeros).  The host picks MAXT =
 // ceil(T_ub / 16), so at most the tiles between T and the bound are idle.
 // The output product is taken transposed (V^T . E^T), so a lane holds four
 // consecutive head dimensions of one query and stores them as 8 bytes.
 constexpr int RES_NT = 512;  // 8 waves share the staged K and V
+// 16-byte staging piece (a vector value, so the staging arrays stay in registers)
+typedef unsigned u32x4v __attribute__((ext_vector_type(4)));
 
 // Long samples (17 .. 37 key tiles, T <= 592: the 384 x 384 workload) use
 // the same kernel with one workgroup per CU: K (74 KB) and V (76 KB) of the
@@ -394,22 +397,23 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
   constexpr int KU = (TP * 8 + RES_NT - 1) / RES_NT;  // 16-byte K pieces per thread
   const bf16_t* kg = qkv + (size_t)base * ld + d + h * 64;
   const bf16_t* vg = qkv + (size_t)base * ld + 2 * d + h * 64;
-  // (rows past the sample read its last row and are replaced by zeros
-  // afterwards, so no load sits behind a branch and they issue together)
-  uint4 kin[KU];
+  // (rows past the sample read its last row, so no load sits behind a
+  // branch and they issue together; those keys keep these finite copies,
+  // whose probabilities are exactly 0 since their key term is -inf)
+  u32x4v kin[KU];
 #pragma unroll
   for (int w = 0; w < KU; w++) {
     const int u = tid + w * RES_NT;
     const int r = u >> 3, cc = (u & 7) * 8;
-    kin[w] = *(const uint4*)(kg + (size_t)min(r, Tn - 1) * ld + cc);
+    kin[w] = *(const u32x4v*)(kg + (size_t)min(r, Tn - 1) * ld + cc);
   }
   constexpr int VU = (TPE * 8 + RES_NT - 1) / RES_NT;  // 16-byte V pieces per thread
-  uint4 vin[VU];
+  u32x4v vin[VU];
 #pragma unroll
   for (int w = 0; w < VU; w++) {
     const int u = tid + w * RES_NT;
     const int r = u >> 3, cc = (u & 7) * 8;
-    vin[w] = *(const uint4*)(vg + (size_t)min(r, Tn - 1) * ld + cc);
+    vin[w] = *(const u32x4v*)(vg + (size_t)min(r, Tn - 1) * ld + cc);
   }
   constexpr int SR = LONG ? (TP + RES_NT - 1) / RES_NT : 1;  // sizes per thread
   float szr[SR];
@@ -420,16 +424,14 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
   for (int w = 0; w < KU; w++) {
     const int u = tid + w * RES_NT;
     if (u < TP * 8)
-      *(uint4*)(Ks + (u >> 3) * 64 + (((u & 7) ^ ((u >> 3) & 7)) << 3)) =
-          (u >> 3) < Tn ? kin[w] : make_uint4(0, 0, 0, 0);
+      *(u32x4v*)(Ks + (u >> 3) * 64 + (((u & 7) ^ ((u >> 3) & 7)) << 3)) = kin[w];
   }
 #pragma unroll
   for (int w = 0; w < VU; w++) {
     const int u = tid + w * RES_NT;
     const int r = u >> 3;
     if (u < TPE * 8)
-      *(uint4*)(Vs + r * 64 + (((u & 7) ^ (((r >> 1) & 1) << 1)) << 3)) =
-          r < Tn ? vin[w] : make_uint4(0, 0, 0, 0);
+      *(u32x4v*)(Vs + r * 64 + (((u & 7) ^ (((r >> 1) & 1) << 1)) << 3)) = vin[w];
   }
   // key term of the base-2 scores: log2(size) (0 without proportional
   // attention), -inf past the sample's keys
@@ -444,14 +446,14 @@ __global__ __launch_bounds__(RES_NT, MAXT <= 16 ? 4 : 1) void attention_mfma_res
   bf16_t* out = (bf16_t*)a.out;
   const bool want_cls = a.cls_scores != nullptr;
   // Q^T operand of the wave's first query tile; the next tile's is fetched
-  // while the current one is processed
+  // while the current one is processed (queries past the sample read its
+  // last row: their rows are computed and never stored)
   uint4 qnext[2];
   auto load_q = [&](int qt, uint4* dstq) {
-    const int q = qt * 16 + c;
+    const int q = min(qt * 16 + c, Tn - 1);
     const bf16_t* qr = qkv + (size_t)(base + q) * ld + h * 64;
 #pragma unroll
-    for (int hf = 0; hf < 2; hf++)
-      dstq[hf] = (q < Tn) ? *(const uint4*)(qr + hf * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
+    for (int hf = 0; hf < 2; hf++) dstq[hf] = *(const uint4*)(qr + hf * 32 + 8 * g);
   };
   load_q(wave, qnext);
   for (int qt = wave; qt < nkt; qt += RES_NT / 64) {
