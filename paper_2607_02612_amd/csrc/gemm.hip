@@ -144,6 +144,7 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // element q of lane l is C[8*(q/4) + 4*(l/32) + q%4][l%32].
 constexpr int NB = 128;
 constexpr int NXCD = 8;
+constexpr long THIN_TILES = 768;
 
 // 16-byte chunk c of staged row r (64-byte rows: four chunks)
 __device__ __forceinline__ int kslot(int r, int c) { return c ^ ((r >> 2) & 3); }
@@ -167,10 +168,13 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
-// MB = 256 (8 waves, 4x2), 128 (4 waves, 2x2) or 64 (2 waves, 1x2) rows per
-// tile.  KSV = K step (32).
-template <int EPI, int MB, int KSV>
-__global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf16(
+// MB = 256, 128 or 64 rows per tile; each wave owns WR * 32 rows x 64
+// columns (WR = 2: 2 x 2 MFMA blocks, WR = 1: 1 x 2), the waves in a grid of
+// MB / (32 WR) rows x 2 columns.  Every layout accumulates each output
+// element over the same 16-wide K pieces in the same order from the same
+// bias start, so the results do not depend on MB or WR.  KSV = K step (32).
+template <int EPI, int MB, int KSV, int WR>
+__global__ __launch_bounds__(MB / (32 * WR) * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf16(
     const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ W,
     int N, int K, const int* M_dev, int M_host, int n_mt, Epi e) {
   static_assert(KSV == 32, "K step of 32");
@@ -178,7 +182,9 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   constexpr int ROWB = KS * 2;                        // bytes per staged row
   constexpr int CPR = KS / 8;                         // 16-byte chunks per staged row
   constexpr int RPI = 64 / CPR;                       // rows per DMA instruction
-  constexpr int NWV = MB / 64 * 2;                    // waves
+  static_assert(WR == 1 || WR == 2, "32 or 64 rows per wave");
+  constexpr int WMR = 32 * WR;                        // rows per wave
+  constexpr int NWV = MB / WMR * 2;                   // waves
   constexpr int NT = NWV * 64;                        // threads
   constexpr int STGB = (MB + NB) * ROWB;              // bytes per stage
   constexpr int DMA_PER_WAVE = (MB + NB) / RPI / NWV; // DMA instructions per wave and stage
@@ -200,7 +206,7 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   // (the column base is clamped as a whole: with N % 8 == 0 the lane
   // halves' columns c and c + 4 stay inside the bias vector; each
   // accumulator set loads its own copy, which costs no vector ALU moves)
-  f32x16_t acc[2][2];
+  f32x16_t acc[WR][2];
   const float* bias_l = e.bias + 4 * (lane >> 5);
 #pragma unroll
   for (int j = 0; j < 2; j++)
@@ -208,7 +214,7 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
     for (int q4 = 0; q4 < 4; q4++) {
       const int cb = min(n0 + wn * 64 + j * 32 + 8 * q4, N - 8);
 #pragma unroll
-      for (int i = 0; i < 2; i++) {
+      for (int i = 0; i < WR; i++) {
         const float4 bv = *(const float4*)(bias_l + cb);
         acc[i][j][4 * q4 + 0] = bv.x;
         acc[i][j][4 * q4 + 1] = bv.y;
@@ -315,8 +321,8 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
       bf16x8_t a[2], b[2];
       const int c = (ks >> 3) + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 2; i++) {
-        const int r = wm * 64 + i * 32 + (lane & 31);
+      for (int i = 0; i < WR; i++) {
+        const int r = wm * WMR + i * 32 + (lane & 31);
         a[i] = *(const bf16x8_t*)(Ab + r * ROWB + (kslot(r, c) << 4));
       }
 #pragma unroll
@@ -327,7 +333,7 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
       // transposed product: acc[i][j] holds C^T, so lane l owns output row
       // m = .. + (l % 32) and columns n = .. + 8 (q / 4) + 4 (l / 32) + q % 4
 #pragma unroll
-      for (int i = 0; i < 2; i++)
+      for (int i = 0; i < WR; i++)
 #pragma unroll
         for (int j = 0; j < 2; j++)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[j], a[i], acc[i][j], 0, 0, 0);
@@ -351,7 +357,7 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
     constexpr int SROW = PAD ? NB * 2 + 16 : NB * 2;
     static_assert(MB * SROW <= NSTG * STGB, "epilogue staging fits");
     __syncthreads();
-    char* sl = smem + (wm * 64 + (lane & 31)) * SROW + (PAD ? wn * 128 + (lane >> 5) * 8 : 0);
+    char* sl = smem + (wm * WMR + (lane & 31)) * SROW + (PAD ? wn * 128 + (lane >> 5) * 8 : 0);
 #pragma unroll
     for (int j = 0; j < 2; j++) {
 #pragma unroll
@@ -360,7 +366,7 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
         // same side of N, so the check is uniform)
         if (n0 + wn * 64 + j * 32 + 8 * q4 >= N) continue;
 #pragma unroll
-        for (int i = 0; i < 2; i++) {
+        for (int i = 0; i < WR; i++) {
           float v0 = acc[i][j][4 * q4 + 0], v1 = acc[i][j][4 * q4 + 1];
           float v2 = acc[i][j][4 * q4 + 2], v3 = acc[i][j][4 * q4 + 3];
           if (EPI == EPI_GELU) {
@@ -370,7 +376,7 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
           if (PAD) {
             *(uint2*)(sl + i * 32 * SROW + j * 64 + q4 * 16) = pk;
           } else {
-            const int r = wm * 64 + i * 32 + (lane & 31);
+            const int r = wm * WMR + i * 32 + (lane & 31);
             const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
             *(uint2*)(smem + r * SROW + (((c >> 3) ^ (r & 15)) << 4) + ((c >> 2) & 1) * 8) = pk;
           }
@@ -405,12 +411,12 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
 #pragma unroll
     for (int rb = 0; rb < MB; rb += RR) {
       __syncthreads();
-      if (wm * 64 >= rb && wm * 64 < rb + RR) {
+      if (wm * WMR >= rb && wm * WMR < rb + RR) {
 #pragma unroll
         for (int j = 0; j < 2; j++) {
 #pragma unroll
-          for (int i = 0; i < 2; i++) {
-            const int r = wm * 64 + i * 32 + (lane & 31) - rb;
+          for (int i = 0; i < WR; i++) {
+            const int r = wm * WMR + i * 32 + (lane & 31) - rb;
 #pragma unroll
             for (int q4 = 0; q4 < 4; q4++) {
               const int c = wn * 64 + j * 32 + 8 * q4 + 4 * (lane >> 5);
@@ -456,8 +462,8 @@ __global__ __launch_bounds__(MB / 64 * 128, MB == 128 ? 3 : 1) void gemm_mfma_bf
   // residual update (other tile heights), fp32 logits (row scatter) and the
   // patch embedding: direct vector accesses
 #pragma unroll
-  for (int i = 0; i < 2; i++) {
-    const int m = m0 + wm * 64 + i * 32 + (lane & 31);
+  for (int i = 0; i < WR; i++) {
+    const int m = m0 + wm * WMR + i * 32 + (lane & 31);
     if (m >= M) continue;
     size_t orow = (size_t)m;
     int pj = 0;
@@ -537,13 +543,18 @@ hipError_t launch_gemm<bf16_t>(const bf16_t* A, int lda, const bf16_t* W,
   const int mb = small ? 64 : big ? 256 : 128;
   const int n_mt = (M_ub + mb - 1) / mb;
   const int grid = (n_mt + NXCD - 1) / NXCD * NXCD * n_nt;
-#define FUSION_GEMM_LAUNCH(E)                                                                 \
-  if (small)                                                                                 \
-    gemm_mfma_bf16<E, 64, 32><<<grid, 128, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
-  else if (big)                                                                              \
-    gemm_mfma_bf16<E, 256, 32><<<grid, 512, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
-  else                                                                                       \
-    gemm_mfma_bf16<E, 128, 32><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e)
+  // 32-row waves (twice the waves per tile) for 64-row tiles when the
+  // launch has fewer tiles than the CUs hold at once
+  const bool thin = small && (long)n_mt * n_nt < THIN_TILES;
+#define FUSION_GEMM_LAUNCH(E)                                                                    \
+  if (small && thin)                                                                            \
+    gemm_mfma_bf16<E, 64, 32, 1><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
+  else if (small)                                                                               \
+    gemm_mfma_bf16<E, 64, 32, 2><<<grid, 128, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
+  else if (big)                                                                                 \
+    gemm_mfma_bf16<E, 256, 32, 2><<<grid, 512, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e); \
+  else                                                                                          \
+    gemm_mfma_bf16<E, 128, 32, 2><<<grid, 256, 0, s>>>(A, lda, W, N, K, M_dev, M_host, n_mt, e)
   switch (e.mode) {
     case EPI_STORE: FUSION_GEMM_LAUNCH(EPI_STORE); break;
     case EPI_GELU: FUSION_GEMM_LAUNCH(EPI_GELU); break;
