@@ -102,7 +102,8 @@ __global__ __launch_bounds__(256) void gemm_valu(const T* __restrict__ A,
 // ------------------------------------------------------------ bf16 MFMA --
 // MBx128 output tile per workgroup (MB = 256: 8 waves in a 4x2 grid; 128: 4
 // waves, 2x2; 64: 2 waves side by side), each wave a 64x64 sub-tile of 2x2
-// v_mfma_f32_32x32x16_bf16 blocks.
+// v_mfma_f32_32x32x16_bf16 blocks; launches with few 64-row tiles split
+// each into 4 waves of 32x64 (1x2 blocks) instead, which changes no result.
 //
 // K is consumed in steps of KSV = 32 through a ring of three LDS stages
 // (64-wide steps with two stages measured slower on every shape, long K
